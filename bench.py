@@ -1,0 +1,180 @@
+#!/usr/bin/env python3
+"""Benchmark: Efficient-Adam rounds per second on one MI355X.
+
+One "step" is one full round (ea_step): N worker compressions, the server's
+dequantize-average + Adam, the server compression and the update of x, on the
+BERT-base-sized workload (d = 110,000,000, N = 16, stochastic 4-bit with L2
+bucket scale, bucket 512, two-way error feedback) unless --workload says
+otherwise.  Inputs are synthetic (workloads.py) and already in HBM when the
+timed region starts; the N gradient buffers are generated once and reused.
+
+Prints ONE JSON line.  `roofline` covers the dominant kernel (step_kernel,
+the only kernel of a bucketed round): achieved = algorithmic HBM bytes per
+round / mean round time from HIP events on the launch stream.
+`cpu_baseline` times the oracle (single-threaded C) on a bounded sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "Efficient-Adam step throughput (Gparam/s, N workers) + % of HBM peak GB/s"
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2205_14473_amd", "csrc", f)
+                  for f in ("ea_kernels.hip", "ea_device.hpp", "ea_launch.hpp", "ea_api.cpp")]
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(E, cfg) -> int:
+    """Minimum HBM bytes of one fused round: every vector crosses HBM once
+    in each direction it must, messages are written once."""
+    d, N = cfg.d, cfg.N
+    ww, sw = E.ea_msg_words(cfg.qw, d), E.ea_msg_words(cfg.qs, d)
+    nw, ns = E.ea_msg_scales(cfg.qw, d), E.ea_msg_scales(cfg.qs, d)
+    if cfg.placement == E.EA_ADAM_AT_SERVER:
+        worker = 12 * d          # read g, read e_w, write e_w
+        server = 32 * d          # m, v, e_s, x: read + write
+    else:
+        worker = 28 * d          # g; e_w, m_w, v_w read + write
+        server = 16 * d          # e_s, x: read + write
+    return N * (worker + 8 * ww + 4 * nw) + server + 8 * sw + 4 * ns
+
+
+def traffic_from_profile(workload: str, placement: str):
+    """HBM bytes per launch measured by rocprofv3 counters, if the committed
+    counter summary was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"step_kernel_{workload}_{placement}_pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_digest") != source_digest():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(E, w, cfg, rb, sample):
+    """The oracle, as it stands, on the first `sample` parameters (one round)."""
+    import numpy as np
+    import oracle as O
+    n = min(sample, cfg.d)
+    B = max(O.bucket_len(O.Quant(**w.qw.fields()), cfg.d), O.bucket_len(O.Quant(**w.qs.fields()), cfg.d))
+    if B < cfg.d:
+        n = max(B, n // B * B)
+    else:
+        n = cfg.d
+    oc = O.Config(d=cfg.d, N=cfg.N, placement=cfg.placement, beta1=cfg.beta1, beta2=cfg.beta2, lr=cfg.lr,
+                  eps=cfg.eps, seed=cfg.seed, qw=O.Quant(**w.qw.fields()), qs=O.Quant(**w.qs.fields()))
+    g = np.ascontiguousarray(rb.g[:, :n].cpu().numpy())
+    st = O.State.init(oc, n, rb.x[:n].cpu().numpy())
+    t0 = time.perf_counter()
+    O.step(oc, 1, g, st, n0=0)
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt / 1e9, 6), "unit": "Gparam/s", "cores": 1, "kind": "oracle",
+            "sample": f"one round over the first {n} of {cfg.d} parameters, N={cfg.N}, single thread, "
+                      f"{dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="bert", choices=[k for k in W.WORKLOADS if k != "toy"])
+    ap.add_argument("--placement", default="server", choices=["server", "worker"])
+    ap.add_argument("--cpu-sample", type=int, default=1 << 24, help="parameters in the oracle's timed sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib-gib", type=float, default=0.0,
+                    help="only run a plain torch copy of this many GiB (HBM counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+
+    if args.copy_calib_gib > 0:
+        n = int(args.copy_calib_gib * (1 << 30)) // 4
+        a = torch.ones(n, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": n * 4, "bytes_written": n * 4}), flush=True)
+        return
+
+    import paper_2205_14473_amd as E
+    from paper_2205_14473_amd.state import allocate, init_state
+
+    w = W.WORKLOADS[args.workload]
+    placement = E.EA_ADAM_AT_SERVER if args.placement == "server" else E.EA_ADAM_AT_WORKER
+    cfg = E.Config(**w.config_fields(placement=placement), qw=E.Quant(**w.qw.fields()), qs=E.Quant(**w.qs.fields()))
+    rb = allocate(cfg)
+    init_state(cfg, rb)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(w.seed)
+    torch.randn(cfg.d, generator=gen, device="cuda", out=rb.x)
+    rb.x.mul_(0.02)
+    W.device_gradients(w, 1, rb.g)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    t = 1
+    for _ in range(args.warmup):
+        E.ea_step(cfg, t, **rb.step_args(), stream=stream)
+        t += 1
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        E.ea_step(cfg, t, **rb.step_args(), stream=stream)
+        t += 1
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+
+    alg = algorithmic_bytes(E, cfg)
+    achieved = alg / (ms * 1e-3) / 1e9
+    value = cfg.d / (ms * 1e-3) / 1e9
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(args.workload, args.placement),
+            "kernel": "step_kernel", "algorithmic_bytes_per_launch": alg,
+            "bytes_per_param": round(alg / cfg.d, 2)}
+    line = {
+        "metric": METRIC, "value": round(value, 4), "unit": "Gparam/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "d": cfg.d, "N": cfg.N,
+                   "placement": "adam_at_server" if placement == 0 else "adam_at_worker",
+                   "qw": w.qw.fields(), "qs": w.qs.fields()},
+        "param_workers_per_s": round(cfg.N * value, 3),
+        "hbm_frac": round(achieved / PEAK_HBM_GBS, 4),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(E, w, cfg, rb, args.cpu_sample)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,482 @@
+// ea_api.cpp -- the C ABI of libea (declared in include/ea.h): argument
+// validation, launch geometry and kernel dispatch on the caller's stream.
+// No entry point allocates memory or synchronizes.
+#include "ea.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "ea_launch.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok()
+{
+    g_err[0] = '\0';
+    return EA_OK;
+}
+
+bool kind_has_scales(int32_t kind)
+{
+    return kind == EA_Q_SCALED_SIGN || kind == EA_Q_STOCH_UNIFORM || kind == EA_Q_DET_UNIFORM;
+}
+
+// Code width of a quantizer (validated), or a negative error.
+int32_t bits_of(const ea_quant_t* q)
+{
+    if (!q) return EA_ERR_ARG;
+    switch (q->kind) {
+    case EA_Q_NONE:
+        return 32;
+    case EA_Q_SCALED_SIGN:
+        return 1;
+    case EA_Q_STOCH_UNIFORM:
+        return (q->bits == 1 || q->bits == 2 || q->bits == 4 || q->bits == 8) ? q->bits : EA_ERR_ARG;
+    case EA_Q_DET_UNIFORM:
+        return (q->bits >= 2 && q->bits <= 8) ? q->bits : EA_ERR_ARG;
+    case EA_Q_POW2: {
+        if (q->pow2_kmin < -126 || q->pow2_kmax > 127 || q->pow2_kmin >= q->pow2_kmax) return EA_ERR_ARG;
+        int32_t need = q->pow2_kmax - q->pow2_kmin + 2;  // exponents plus the zero code
+        int32_t b = 0;
+        while ((1 << b) < need) ++b;
+        return 1 + b;
+    }
+    default:
+        return EA_ERR_ARG;
+    }
+}
+
+bool one_bucket(const ea_quant_t* q, int64_t d)
+{
+    return kind_has_scales(q->kind) && (q->bucket <= 0 || q->bucket >= d);
+}
+
+int64_t bucket_len(const ea_quant_t* q, int64_t d)
+{
+    return one_bucket(q, d) ? d : q->bucket;
+}
+
+int64_t nscales_of(const ea_quant_t* q, int64_t d)
+{
+    if (!kind_has_scales(q->kind)) return 0;
+    const int64_t B = bucket_len(q, d);
+    return (d + B - 1) / B;
+}
+
+int64_t words_of(int32_t b, int64_t d)
+{
+    return b == 32 ? (d + 1) / 2 : ((d + 255) / 256) * 4 * b;
+}
+
+int check_quant(const ea_quant_t* q, int64_t d, const char* side)
+{
+    const int32_t b = bits_of(q);
+    if (b < 0) return fail(EA_ERR_ARG, "%s quantizer: invalid kind %d / bits %d / pow2 range [%d, %d]", side,
+                           q->kind, q->bits, q->pow2_kmin, q->pow2_kmax);
+    if (q->kind == EA_Q_STOCH_UNIFORM && q->scale != EA_SCALE_L2 && q->scale != EA_SCALE_MAX)
+        return fail(EA_ERR_ARG, "%s quantizer: stochastic uniform needs EA_SCALE_L2 or EA_SCALE_MAX", side);
+    if (q->error_feedback != 0 && q->error_feedback != 1)
+        return fail(EA_ERR_ARG, "%s quantizer: error_feedback must be 0 or 1", side);
+    if (q->bucket < 0) return fail(EA_ERR_ARG, "%s quantizer: negative bucket", side);
+    if (kind_has_scales(q->kind) && !one_bucket(q, d)) {
+        const int64_t B = q->bucket;
+        if (B != 256 && B != 512 && B != 1024 && B != 2048)
+            return fail(EA_ERR_UNSUPPORTED, "%s quantizer: bucket %lld must be 256, 512, 1024, 2048, 0 or >= d",
+                        side, (long long)B);
+    }
+    return EA_OK;
+}
+
+struct Plan {
+    int C;                 // chunks per tile
+    int64_t ntiles;
+    ea::QDev qw, qs;
+    bool wglobal, sglobal; // one-bucket quantizers
+    int64_t off_wpart, off_spart, off_ubuf, ws_bytes;
+};
+
+ea::QDev make_qdev(const ea_quant_t* q, int64_t d)
+{
+    ea::QDev r{};
+    r.kind = q->kind;
+    r.bits = bits_of(q);
+    r.ef = q->error_feedback;
+    r.norm = q->kind == EA_Q_SCALED_SIGN ? ea::S_L1
+           : (q->kind == EA_Q_STOCH_UNIFORM && q->scale == EA_SCALE_L2) ? ea::S_L2 : ea::S_MAX;
+    r.B = kind_has_scales(q->kind) ? bucket_len(q, d) : d;
+    r.cpb = (kind_has_scales(q->kind) && !one_bucket(q, d)) ? (int32_t)(q->bucket / 256) : 0;
+    r.L = q->kind == EA_Q_STOCH_UNIFORM ? (1 << r.bits) - 1 : q->kind == EA_Q_DET_UNIFORM ? (1 << (r.bits - 1)) - 1 : 0;
+    r.kmin = q->pow2_kmin;
+    r.kmax = q->pow2_kmax;
+    r.nscales = nscales_of(q, d);
+    r.words = words_of(r.bits, d);
+    return r;
+}
+
+int64_t align256(int64_t x)
+{
+    return (x + 255) / 256 * 256;
+}
+
+int validate(const ea_config_t* c)
+{
+    if (!c) return fail(EA_ERR_ARG, "config is NULL");
+    if (c->d < 1) return fail(EA_ERR_ARG, "d must be >= 1 (got %lld)", (long long)c->d);
+    if (c->d > ((int64_t)1 << 40)) return fail(EA_ERR_UNSUPPORTED, "d above 2^40 is not supported");
+    if (c->N < 1 || c->N > 1024) return fail(EA_ERR_ARG, "N must be in [1, 1024] (got %d)", c->N);
+    if (c->placement != EA_ADAM_AT_SERVER && c->placement != EA_ADAM_AT_WORKER)
+        return fail(EA_ERR_ARG, "placement must be EA_ADAM_AT_SERVER or EA_ADAM_AT_WORKER");
+    if (!(c->beta1 >= 0.0f && c->beta1 < 1.0f)) return fail(EA_ERR_ARG, "beta1 must be in [0, 1)");
+    if (!(c->beta2 >= 0.0f && c->beta2 < 1.0f)) return fail(EA_ERR_ARG, "beta2 must be in [0, 1)");
+    if (!std::isfinite(c->lr)) return fail(EA_ERR_ARG, "lr must be finite");
+    if (!(c->eps >= 0.0f) || !std::isfinite(c->eps)) return fail(EA_ERR_ARG, "eps must be finite and >= 0");
+    int rc = check_quant(&c->qw, c->d, "worker");
+    if (rc) return rc;
+    return check_quant(&c->qs, c->d, "server");
+}
+
+int make_plan(const ea_config_t* c, Plan* p)
+{
+    int rc = validate(c);
+    if (rc) return rc;
+    p->qw = make_qdev(&c->qw, c->d);
+    p->qs = make_qdev(&c->qs, c->d);
+    const int cw = p->qw.cpb, cs = p->qs.cpb;
+    p->C = cw > cs ? cw : cs;
+    if (p->C == 0) p->C = 2;
+    const int64_t tile = (int64_t)p->C * ea::kChunk;
+    p->ntiles = (c->d + tile - 1) / tile;
+    p->wglobal = kind_has_scales(c->qw.kind) && cw == 0;
+    p->sglobal = kind_has_scales(c->qs.kind) && cs == 0;
+    int64_t off = 0;
+    p->off_wpart = off;
+    if (p->wglobal) off += align256((int64_t)c->N * p->ntiles * 8);
+    p->off_spart = off;
+    if (p->sglobal) off += align256(p->ntiles * 8);
+    p->off_ubuf = off;
+    if (p->sglobal) off += align256(c->d * 4);
+    p->ws_bytes = off;
+    return EA_OK;
+}
+
+bool aligned(const void* ptr, uintptr_t a)
+{
+    return ((uintptr_t)ptr % a) == 0;
+}
+
+// Fills the common part of the kernel argument block.
+ea::StepArgs base_args(const ea_config_t* c, const Plan& p, int64_t t)
+{
+    ea::StepArgs a{};
+    a.d = c->d;
+    a.N = c->N;
+    a.placement = c->placement;
+    a.beta1 = c->beta1;
+    a.beta2 = c->beta2;
+    a.lr = c->lr;
+    a.k0 = (uint32_t)c->seed;
+    a.k1 = (uint32_t)(c->seed >> 32);
+    a.t = (uint32_t)t;
+    a.ntiles = p.ntiles;
+    a.qw = p.qw;
+    a.qs = p.qs;
+    return a;
+}
+
+int check_t(int64_t t)
+{
+    if (t < 1 || t > (int64_t)0xFFFFFFFFLL) return fail(EA_ERR_ARG, "t must be in [1, 2^32-1] (got %lld)", (long long)t);
+    return EA_OK;
+}
+
+int hip_status(hipError_t e, const char* what)
+{
+    if (e != hipSuccess) return fail(EA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+struct PtrCheck {
+    int rc = EA_OK;
+    void need(const void* ptr, bool required, uintptr_t align, const char* name)
+    {
+        if (rc) return;
+        if (!ptr) {
+            if (required) rc = fail(EA_ERR_ARG, "%s is NULL", name);
+            return;
+        }
+        if (!aligned(ptr, align)) rc = fail(EA_ERR_ALIGN, "%s is not %u-byte aligned", name, (unsigned)align);
+    }
+};
+
+// Vector path when every float row is 16-byte aligned.
+bool vec_ok(int64_t d, std::initializer_list<const void*> ptrs)
+{
+    if (d % 4) return false;
+    for (const void* q : ptrs)
+        if (q && !aligned(q, 16)) return false;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t ea_code_bits(const ea_quant_t* q)
+{
+    const int32_t b = bits_of(q);
+    if (b < 0) return fail(b, "invalid quantizer description");
+    return b;
+}
+
+int64_t ea_msg_words(const ea_quant_t* q, int64_t d)
+{
+    const int32_t b = bits_of(q);
+    if (b < 0 || d < 1) return fail(EA_ERR_ARG, "invalid quantizer or d");
+    return words_of(b, d);
+}
+
+int64_t ea_msg_scales(const ea_quant_t* q, int64_t d)
+{
+    if (bits_of(q) < 0 || d < 1) return fail(EA_ERR_ARG, "invalid quantizer or d");
+    return nscales_of(q, d);
+}
+
+int64_t ea_msg_bits(const ea_quant_t* q, int64_t d)
+{
+    const int32_t b = bits_of(q);
+    if (b < 0 || d < 1) return fail(EA_ERR_ARG, "invalid quantizer or d");
+    return d * b + 32 * nscales_of(q, d);
+}
+
+int64_t ea_workspace_bytes(const ea_config_t* c)
+{
+    Plan p;
+    const int rc = make_plan(c, &p);
+    if (rc) return rc;
+    return p.ws_bytes;
+}
+
+int ea_validate(const ea_config_t* c)
+{
+    Plan p;
+    const int rc = make_plan(c, &p);
+    return rc ? rc : ok();
+}
+
+const char* ea_last_error(void)
+{
+    return g_err;
+}
+
+int ea_state_init(const ea_config_t* c, float* m, float* v, float* e_s, float* e_w, float* m_w, float* v_w,
+                  void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    const bool srv = c->placement == EA_ADAM_AT_SERVER;
+    PtrCheck pc;
+    pc.need(e_s, true, 4, "e_s");
+    pc.need(e_w, true, 4, "e_w");
+    pc.need(m, srv, 4, "m");
+    pc.need(v, srv, 4, "v");
+    pc.need(m_w, !srv, 4, "m_w");
+    pc.need(v_w, !srv, 4, "v_w");
+    if (pc.rc) return pc.rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t d = c->d, Nd = (int64_t)c->N * c->d;
+    hipError_t e = ea::launch_fill(e_s, d, 0.0f, s);
+    if (e == hipSuccess) e = ea::launch_fill(e_w, Nd, 0.0f, s);
+    if (e == hipSuccess && srv) e = ea::launch_fill(m, d, 0.0f, s);
+    if (e == hipSuccess && srv) e = ea::launch_fill(v, d, c->eps, s);
+    if (e == hipSuccess && !srv) e = ea::launch_fill(m_w, Nd, 0.0f, s);
+    if (e == hipSuccess && !srv) e = ea::launch_fill(v_w, Nd, c->eps, s);
+    return hip_status(e, "ea_state_init");
+}
+
+int ea_worker_compress(const ea_config_t* c, int32_t i, int64_t t, const float* g, float* e_w, float* m_w,
+                       float* v_w, uint64_t* codes, float* scales, void* workspace, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    if ((rc = check_t(t))) return rc;
+    if (i < 0 || i >= c->N) return fail(EA_ERR_ARG, "worker index %d outside [0, %d)", i, c->N);
+    const bool atw = c->placement == EA_ADAM_AT_WORKER;
+    PtrCheck pc;
+    pc.need(g, true, 4, "g");
+    pc.need(e_w, true, 4, "e_w");
+    pc.need(m_w, atw, 4, "m_w");
+    pc.need(v_w, atw, 4, "v_w");
+    pc.need(codes, true, 8, "codes");
+    pc.need(scales, p.qw.nscales > 0, 4, "scales");
+    pc.need(workspace, p.wglobal, 256, "workspace");
+    if (pc.rc) return pc.rc;
+    ea::StepArgs a = base_args(c, p, t);
+    a.g = g;
+    a.e_w = e_w;
+    a.m_w = atw ? m_w : nullptr;
+    a.v_w = atw ? v_w : nullptr;
+    a.wcodes = codes;
+    a.wscales = scales;
+    a.worker = i;
+    const bool vec = vec_ok(c->d, {g, e_w, a.m_w, a.v_w});
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipSuccess;
+    if (p.wglobal) {
+        a.wpart = (double*)((char*)workspace + p.off_wpart);
+        e = ea::launch_worker_partials(a, p.C, vec, i, i + 1, s);
+        if (e == hipSuccess) e = ea::launch_finalize(a.wpart, p.ntiles, p.qw.norm, c->d, scales, 1, 1, s);
+    }
+    if (e == hipSuccess) e = ea::launch_worker(a, p.C, vec, s);
+    return hip_status(e, "ea_worker_compress");
+}
+
+int ea_server_aggregate_adam(const ea_config_t* c, int64_t t, const uint64_t* wcodes, const float* wscales,
+                             float* m, float* v, float* u_out, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    if ((rc = check_t(t))) return rc;
+    const bool srv = c->placement == EA_ADAM_AT_SERVER;
+    PtrCheck pc;
+    pc.need(wcodes, true, 8, "wcodes");
+    pc.need(wscales, p.qw.nscales > 0, 4, "wscales");
+    pc.need(m, srv, 4, "m");
+    pc.need(v, srv, 4, "v");
+    pc.need(u_out, true, 4, "u_out");
+    if (pc.rc) return pc.rc;
+    ea::StepArgs a = base_args(c, p, t);
+    a.wcodes = const_cast<uint64_t*>(wcodes);
+    a.wscales = const_cast<float*>(wscales);
+    a.m = srv ? m : nullptr;
+    a.v = srv ? v : nullptr;
+    a.ubuf = u_out;
+    const bool vec = vec_ok(c->d, {a.m, a.v, u_out});
+    return hip_status(ea::launch_aggregate(a, p.C, vec, (hipStream_t)stream), "ea_server_aggregate_adam");
+}
+
+int ea_server_compress(const ea_config_t* c, int64_t t, const float* u, float* e_s, uint64_t* codes,
+                       float* scales, void* workspace, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    if ((rc = check_t(t))) return rc;
+    PtrCheck pc;
+    pc.need(u, true, 4, "u");
+    pc.need(e_s, true, 4, "e_s");
+    pc.need(codes, true, 8, "codes");
+    pc.need(scales, p.qs.nscales > 0, 4, "scales");
+    pc.need(workspace, p.sglobal, 256, "workspace");
+    if (pc.rc) return pc.rc;
+    ea::StepArgs a = base_args(c, p, t);
+    a.ubuf = const_cast<float*>(u);
+    a.e_s = e_s;
+    a.scodes = codes;
+    a.sscales = scales;
+    a.apply = 0;
+    const bool vec = vec_ok(c->d, {u, e_s});
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipSuccess;
+    if (p.sglobal) {
+        a.spart = (double*)((char*)workspace + p.off_spart);
+        e = ea::launch_server_partials(a, p.C, vec, s);
+        if (e == hipSuccess) e = ea::launch_finalize(a.spart, p.ntiles, p.qs.norm, c->d, scales, 1, 1, s);
+    }
+    if (e == hipSuccess) e = ea::launch_server(a, p.C, vec, s);
+    return hip_status(e, "ea_server_compress");
+}
+
+int ea_worker_apply(const ea_config_t* c, const uint64_t* codes, const float* scales, float* x, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    PtrCheck pc;
+    pc.need(codes, true, 8, "codes");
+    pc.need(scales, p.qs.nscales > 0, 4, "scales");
+    pc.need(x, true, 4, "x");
+    if (pc.rc) return pc.rc;
+    ea::StepArgs a = base_args(c, p, 1);
+    a.scodes = const_cast<uint64_t*>(codes);
+    a.sscales = const_cast<float*>(scales);
+    a.x = x;
+    const bool vec = vec_ok(c->d, {x});
+    return hip_status(ea::launch_apply(a, p.C, vec, (hipStream_t)stream), "ea_worker_apply");
+}
+
+int ea_step(const ea_config_t* c, int64_t t, const float* g, float* e_w, float* m_w, float* v_w, float* m,
+            float* v, float* e_s, float* x, uint64_t* wcodes, float* wscales, uint64_t* scodes, float* sscales,
+            void* workspace, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    if ((rc = check_t(t))) return rc;
+    const bool srv = c->placement == EA_ADAM_AT_SERVER;
+    PtrCheck pc;
+    pc.need(g, true, 4, "g");
+    pc.need(e_w, true, 4, "e_w");
+    pc.need(m_w, !srv, 4, "m_w");
+    pc.need(v_w, !srv, 4, "v_w");
+    pc.need(m, srv, 4, "m");
+    pc.need(v, srv, 4, "v");
+    pc.need(e_s, true, 4, "e_s");
+    pc.need(x, true, 4, "x");
+    pc.need(wcodes, true, 8, "wcodes");
+    pc.need(wscales, p.qw.nscales > 0, 4, "wscales");
+    pc.need(scodes, true, 8, "scodes");
+    pc.need(sscales, p.qs.nscales > 0, 4, "sscales");
+    pc.need(workspace, p.ws_bytes > 0, 256, "workspace");
+    if (pc.rc) return pc.rc;
+    ea::StepArgs a = base_args(c, p, t);
+    a.g = g;
+    a.e_w = e_w;
+    a.m_w = srv ? nullptr : m_w;
+    a.v_w = srv ? nullptr : v_w;
+    a.m = srv ? m : nullptr;
+    a.v = srv ? v : nullptr;
+    a.e_s = e_s;
+    a.x = x;
+    a.wcodes = wcodes;
+    a.wscales = wscales;
+    a.scodes = scodes;
+    a.sscales = sscales;
+    a.apply = 1;
+    if (p.wglobal) a.wpart = (double*)((char*)workspace + p.off_wpart);
+    if (p.sglobal) {
+        a.spart = (double*)((char*)workspace + p.off_spart);
+        a.ubuf = (float*)((char*)workspace + p.off_ubuf);
+    }
+    const bool vec = vec_ok(c->d, {g, e_w, a.m_w, a.v_w, a.m, a.v, e_s, x, a.ubuf});
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipSuccess;
+    if (p.wglobal) {
+        e = ea::launch_worker_partials(a, p.C, vec, 0, c->N, s);
+        if (e == hipSuccess)
+            e = ea::launch_finalize(a.wpart, p.ntiles, p.qw.norm, c->d, wscales, p.qw.nscales, c->N, s);
+    }
+    if (e == hipSuccess) e = ea::launch_step(a, p.C, vec, s);
+    if (e == hipSuccess && p.sglobal) {
+        e = ea::launch_finalize(a.spart, p.ntiles, p.qs.norm, c->d, sscales, 1, 1, s);
+        if (e == hipSuccess) e = ea::launch_server(a, p.C, vec, s);
+    }
+    return hip_status(e, "ea_step");
+}
+
+}  // extern "C"

@@ -1,0 +1,57 @@
+// ea_launch.hpp -- kernel argument block and launchers shared by the C ABI
+// (ea_api.cpp) and the kernels (ea_kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ea_device.hpp"
+
+namespace ea {
+
+// Everything one launch needs; pointers are device memory.
+struct StepArgs {
+    int64_t d;
+    int32_t N;
+    int32_t placement;
+    float beta1, beta2, lr;
+    uint32_t k0, k1;          // Philox key = seed
+    uint32_t t;               // step (Philox counter word 2)
+    int64_t ntiles;           // tiles of C chunks covering d
+    QDev qw, qs;
+    // worker side ([N][d] in ea_step; one row in the split calls)
+    const float* g;
+    float* e_w;
+    float* m_w;
+    float* v_w;
+    // server side ([d])
+    float* m;
+    float* v;
+    float* e_s;
+    float* x;
+    // messages
+    uint64_t* wcodes;         // [N][qw.words]
+    float* wscales;           // [N][qw.nscales]
+    uint64_t* scodes;         // [qs.words]
+    float* sscales;           // [qs.nscales]
+    // one-bucket workspace
+    double* wpart;            // [N][ntiles] per-tile partial norms (qw one bucket)
+    double* spart;            // [ntiles]    per-tile partial norms (qs one bucket)
+    float* ubuf;              // [d] server input / aggregate output
+    int32_t worker;           // split calls: worker index (Philox stream)
+    int32_t apply;            // server_kernel: also update x
+};
+
+// Launchers; C = chunks per tile (1..8), vec = rows are 16-byte aligned.
+hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s);
+hipError_t launch_worker_partials(const StepArgs& a, int C, bool vec, int i0, int i1, hipStream_t s);
+hipError_t launch_server_partials(const StepArgs& a, int C, bool vec, hipStream_t s);
+hipError_t launch_finalize(const double* part, int64_t ntiles, int32_t norm, int64_t n, float* out,
+                           int64_t out_stride, int nvec, hipStream_t s);
+hipError_t launch_worker(const StepArgs& a, int C, bool vec, hipStream_t s);
+hipError_t launch_aggregate(const StepArgs& a, int C, bool vec, hipStream_t s);
+hipError_t launch_server(const StepArgs& a, int C, bool vec, hipStream_t s);
+hipError_t launch_apply(const StepArgs& a, int C, bool vec, hipStream_t s);
+hipError_t launch_fill(float* p, int64_t n, float value, hipStream_t s);
+
+}  // namespace ea

@@ -1,0 +1,122 @@
+"""Host-side checks of the C ABI (no GPU work): every symbol declared in
+include/ea.h is exported, size queries agree with the oracle's independent
+size rules, and invalid calls are rejected before any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def E():
+    from paper_2205_14473_amd import build as bld
+    if bld.is_stale():
+        bld.build()
+    import paper_2205_14473_amd as E
+    return E
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "ea.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ea_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(E):
+    names = _declared()
+    assert len(names) == 13, names
+    for n in names:
+        assert hasattr(E.lib, n), f"{n} declared in include/ea.h but not exported"
+
+
+QUANTS = [
+    dict(kind=0),
+    dict(kind=1, scale=0, bucket=2048),
+    dict(kind=1, bucket=0),
+    dict(kind=2, scale=1, bits=4, bucket=512),
+    dict(kind=2, scale=2, bits=2, bucket=1024),
+    dict(kind=2, scale=2, bits=8, bucket=0),
+    dict(kind=3, bits=2, bucket=0),
+    dict(kind=3, bits=7, bucket=256),
+    dict(kind=4, pow2_kmin=-17, pow2_kmax=-11),
+    dict(kind=4, pow2_kmin=-126, pow2_kmax=127),
+]
+
+
+@pytest.mark.parametrize("qd", QUANTS)
+@pytest.mark.parametrize("d", [1, 255, 256, 257, 65536, 110_000_000, 355_000_001])
+def test_sizes_agree_with_oracle(E, qd, d):
+    qe, qo = E.Quant(**qd), O.Quant(**qd)
+    assert E.ea_code_bits(qe) == O.code_bits(qo)
+    assert E.ea_msg_words(qe, d) == O.msg_words(qo, d)
+    assert E.ea_msg_scales(qe, d) == O.num_scales(qo, d, d)
+    assert E.ea_msg_bits(qe, d) == d * O.code_bits(qo) + 32 * O.num_scales(qo, d, d)
+
+
+def _cfg(E, **kw):
+    q = E.Quant(kind=2, scale=1, bits=4, error_feedback=1, bucket=512)
+    base = dict(d=110_000_000, N=16, placement=0, beta1=0.9, beta2=0.999, lr=1e-3, eps=1e-8, seed=4, qw=q, qs=q)
+    base.update(kw)
+    return E.Config(**base)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("d", 0, -1), ("N", 0, -1), ("N", 1025, -1), ("placement", 2, -1), ("beta1", 1.0, -1),
+    ("beta2", -0.1, -1), ("lr", float("inf"), -1), ("eps", -1.0, -1)])
+def test_invalid_config_rejected(E, field, value, code):
+    assert E.ea_validate(_cfg(E, **{field: value})) == code
+    assert E.ea_last_error() != ""
+
+
+@pytest.mark.parametrize("qd,code", [
+    (dict(kind=9), -1), (dict(kind=2, scale=1, bits=3, bucket=512), -1), (dict(kind=2, scale=0, bits=2), -1),
+    (dict(kind=3, bits=1), -1), (dict(kind=4, pow2_kmin=-3, pow2_kmax=-3), -1),
+    (dict(kind=1, bucket=768), -4), (dict(kind=1, bucket=4096), -4), (dict(kind=1, bucket=-5), -1),
+    (dict(kind=1, error_feedback=2, bucket=512), -1)])
+def test_invalid_quantizer_rejected(E, qd, code):
+    assert E.ea_validate(_cfg(E, qw=E.Quant(**qd))) == code
+    assert E.ea_validate(_cfg(E, qs=E.Quant(**qd))) == code
+
+
+def test_valid_configs_and_workspace(E):
+    assert E.ea_validate(_cfg(E)) == 0
+    assert E.ea_workspace_bytes(_cfg(E)) == 0
+    one = E.Quant(kind=1, bucket=0)
+    ws = E.ea_workspace_bytes(_cfg(E, d=65536, N=4, qw=one, qs=one))
+    # worker partials [N][tiles] + server partials [tiles] + server input [d], 256-byte aligned
+    assert ws == 4 * 128 * 8 + 1024 + 65536 * 4
+
+
+def test_calls_rejected_before_device_work(E):
+    # Uses fake device addresses: only ever run where no GPU is visible, so a
+    # validation bug can never turn into a kernel launch on real memory.
+    torch = pytest.importorskip("torch")
+    if torch.cuda.device_count() > 0:
+        pytest.skip("bogus-pointer rejection test runs on GPU-less hosts only")
+    c = _cfg(E, d=1024, N=2)
+    P = ctypes.c_void_p
+    good = [P(4096 * (k + 1)) for k in range(14)]
+    # NULL pointer
+    assert E.lib.ea_step(ctypes.byref(c), 1, None, *good[1:]) == E.EA_ERR_ARG
+    assert "g is NULL" in E.ea_last_error()
+    # misaligned float pointer
+    args = list(good)
+    args[0] = P(4098)
+    assert E.lib.ea_step(ctypes.byref(c), 1, *args) == E.EA_ERR_ALIGN
+    # step index out of range
+    assert E.lib.ea_step(ctypes.byref(c), 0, *good) == E.EA_ERR_ARG
+    assert E.lib.ea_step(ctypes.byref(c), 2 ** 32, *good) == E.EA_ERR_ARG
+    # worker index out of range
+    assert E.lib.ea_worker_compress(ctypes.byref(c), 2, 1, *good[:8]) == E.EA_ERR_ARG
+    # misaligned code words (need 8 bytes)
+    assert E.lib.ea_worker_apply(ctypes.byref(c), P(4100), P(4096), P(4096), None) == E.EA_ERR_ALIGN
+    # missing workspace for a one-bucket quantizer
+    one = E.Quant(kind=1, bucket=0)
+    c1 = _cfg(E, d=1024, N=2, qw=one, qs=one)
+    assert E.lib.ea_step(ctypes.byref(c1), 1, *good[:12], None, None) == E.EA_ERR_ARG
+    assert "workspace" in E.ea_last_error()

@@ -1,0 +1,116 @@
+"""Full-size parity: each workload at its real d and N through ea_step (the
+launch the benchmark times), checked against the oracle on sampled
+bucket-aligned segments.  Every step is bucket-local, so the oracle run on a
+segment (with its global element offset for the draws) is exactly the slice
+of a full run (pinned on the CPU by test_segment_equals_slice_of_full_run).
+Also: replaying steps from saved state is bit-identical (resume)."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2205_14473_amd as E  # noqa: E402
+from paper_2205_14473_amd.state import allocate, init_state  # noqa: E402
+from parity_util import Stats, _codes_match, _ulp_diff, close, configs  # noqa: E402
+
+
+def _segments(d, tile, count, seed):
+    ntiles = -(-d // tile)
+    rng = np.random.default_rng(seed)
+    picks = set(rng.choice(ntiles, size=min(count, ntiles), replace=False).tolist()) | {0, ntiles - 1}
+    return [(k * tile, min(tile, d - k * tile)) for k in sorted(picks)]
+
+
+@pytest.mark.parametrize("key", ["bert", "resnet18", "resnet50", "gpt2m"])
+def test_full_size_sampled(key):
+    w = W.WORKLOADS[key]
+    print(f"\n[fullsize] {w.name}", flush=True)
+    d, N, T = w.d, w.N, 3
+    oc, ec = configs(d, N, w.qw.fields(), w.qs.fields(), w.placement, w.seed, w.beta1, w.beta2, w.lr, w.eps)
+    rb = allocate(ec)
+    init_state(ec, rb)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(w.seed)
+    torch.randn(d, generator=gen, device="cuda", out=rb.x)
+    rb.x.mul_(0.02)
+    tile = max(O.bucket_len(oc.qw, d), O.bucket_len(oc.qs, d), 512)
+    segs = _segments(d, tile, 24, w.seed)
+    bw, bs = O.code_bits(oc.qw), O.code_bits(oc.qs)
+    Bw, Bs = O.bucket_len(oc.qw, d), O.bucket_len(oc.qs, d)
+    x_host = rb.x.cpu().numpy()
+    states = {n0: O.State.init(oc, ln, x_host[n0:n0 + ln]) for n0, ln in segs}
+    stats = Stats()
+    for t in range(1, T + 1):
+        W.device_gradients(w, t, rb.g)
+        g_host = {n0: rb.g[:, n0:n0 + ln].cpu().numpy() for n0, ln in segs}
+        E.ea_step(ec, t, **rb.step_args())
+        torch.cuda.synchronize()
+        wc, ws, sc, ss = rb.wcodes.cpu(), rb.wscales.cpu(), rb.scodes.cpu(), rb.sscales.cpu()
+        for n0, ln in segs:
+            st = states[n0]
+            out = O.step(oc, t, np.ascontiguousarray(g_host[n0]), st, n0=n0)
+            w0, w1 = n0 // 256 * 4 * bw, n0 // 256 * 4 * bw + out["wcodes"].shape[1]
+            v0, v1 = n0 // 256 * 4 * bs, n0 // 256 * 4 * bs + out["scodes"].shape[0]
+            ws_g = ws[:, n0 // Bw:n0 // Bw + out["wscales"].shape[1]].numpy()
+            ss_g = ss[n0 // Bs:n0 // Bs + out["sscales"].shape[0]].numpy()
+            assert np.all(_ulp_diff(ws_g, out["wscales"]) <= 1) and np.all(_ulp_diff(ss_g, out["sscales"]) <= 1)
+            ties = 0
+            for i in range(N):
+                ties += _codes_match(oc.qw, bw, d, n0, wc[i, w0:w1].numpy(), out["wcodes"][i], ws_g[i],
+                                     out["wscales"][i], stats, f"worker {i} segment {n0}")
+            ties += _codes_match(oc.qs, bs, d, n0, sc[v0:v1].numpy(), out["scodes"], ss_g, out["sscales"], stats,
+                                 f"server segment {n0}")
+            stats.code_ties += ties
+            stats.code_entries += (N + 1) * ln
+            close("e_w", rb.e_w[:, n0:n0 + ln].cpu().numpy(), st.e_w, stats)
+            close("e_s", rb.e_s[n0:n0 + ln].cpu().numpy(), st.e_s, stats)
+            close("x", rb.x[n0:n0 + ln].cpu().numpy(), st.x, stats)
+            close("m", rb.m[n0:n0 + ln].cpu().numpy(), st.m, stats)
+            close("v", rb.v[n0:n0 + ln].cpu().numpy(), st.v, stats)
+            if ties or not np.array_equal(rb.x[n0:n0 + ln].cpu().numpy(), st.x):
+                stats.resyncs += 1     # put the oracle's segment state back on the GPU
+                rb.e_w[:, n0:n0 + ln].copy_(torch.from_numpy(st.e_w))
+                rb.e_s[n0:n0 + ln].copy_(torch.from_numpy(st.e_s))
+                rb.x[n0:n0 + ln].copy_(torch.from_numpy(st.x))
+                rb.m[n0:n0 + ln].copy_(torch.from_numpy(st.m))
+                rb.v[n0:n0 + ln].copy_(torch.from_numpy(st.v))
+    assert stats.code_ties <= 1e-6 * stats.code_entries + 1
+    print(f"[fullsize] {key}: {len(segs)} segments x {T} steps: {stats}", flush=True)
+    del rb
+    torch.cuda.empty_cache()
+
+
+def test_resume_is_bit_identical():
+    """10 steps, save, 10 more == 20 straight (draws depend on (seed, t, n) only)."""
+    w = W.WORKLOADS["bert"]
+    d, N = 512 * 64 + 100, 4
+    _, ec = configs(d, N, w.qw.fields(), w.qs.fields(), O.ADAM_AT_SERVER, 4)
+    grads = [torch.from_numpy(W.host_gradients(W.Workload("r", "r", d, N, None, None, 1, 4, "student_t"), t, d=d))
+             for t in range(1, 21)]
+
+    def run(rb, t0, t1):
+        for t in range(t0, t1):
+            rb.g.copy_(grads[t - 1])
+            E.ea_step(ec, t, **rb.step_args())
+        torch.cuda.synchronize()
+
+    a = allocate(ec)
+    init_state(ec, a)
+    run(a, 1, 21)
+    b = allocate(ec)
+    init_state(ec, b)
+    run(b, 1, 11)
+    saved = {k: getattr(b, k).cpu().clone() for k in ("e_w", "e_s", "x", "m", "v")}
+    c = allocate(ec)
+    for k, val in saved.items():
+        getattr(c, k).copy_(val)
+    run(c, 11, 21)
+    for k in ("e_w", "e_s", "x", "m", "v", "wcodes", "wscales", "scodes", "sscales"):
+        assert np.array_equal(getattr(a, k).cpu().numpy(), getattr(c, k).cpu().numpy()), k

@@ -1,0 +1,135 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle, element by
+element, after every step of a trajectory.  Sizes span several tiles and a
+ragged tail; the comparison rule is in tests/parity_util.py."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU-only host
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from parity_util import Pair, qfields  # noqa: E402
+
+SIGN = lambda b, ef=1: qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, ef, b)  # noqa: E731
+STOCH = lambda bits, sc, b, ef=1: qfields(O.Q_STOCH_UNIFORM, bits, sc, ef, b)  # noqa: E731
+
+
+def _grads(gen, seed, t, N, d):
+    w = W.Workload("t", "t", d, N, None, None, 1, seed, gen)
+    return W.host_gradients(w, t, d=d)
+
+
+def _run(d, N, qw, qs, placement, T, gen="student_t", seed=5, split=False, x1=None, **hp):
+    pair = Pair(d, N, qw, qs, placement, seed=seed, x1=x1, split=split, **hp)
+    for t in range(1, T + 1):
+        pair.step(t, _grads(gen, seed, t, N, d))
+    pair.check_tie_budget()
+    print(f"\n[parity] d={d} N={N} T={T} placement={placement} split={split}: {pair.stats}", flush=True)
+    return pair
+
+
+# The five workload shapes at reduced d (same N, quantizers and buckets; the
+# tails reproduce each workload's last partial bucket / 64-element group).
+SHAPES = {
+    "resnet18": (2048 * 9 + 1576, 8, SIGN(2048), SIGN(2048), "segscale"),
+    "resnet50": (512 * 21 + 40, 32, STOCH(2, O.SCALE_MAX, 512), STOCH(2, O.SCALE_MAX, 512), "segscale"),
+    "bert": (512 * 40 + 384, 16, STOCH(4, O.SCALE_L2, 512), STOCH(4, O.SCALE_L2, 512), "student_t"),
+    "gpt2m": (1024 * 13 + 704, 8, STOCH(2, O.SCALE_MAX, 1024), SIGN(1024), "outliers"),
+}
+
+
+@pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
+@pytest.mark.parametrize("shape", list(SHAPES))
+def test_workload_shapes_fused(shape, placement):
+    d, N, qw, qs, gen = SHAPES[shape]
+    _run(d, N, qw, qs, placement, T=12, gen=gen)
+
+
+@pytest.mark.parametrize("shape", list(SHAPES))
+def test_workload_shapes_split_calls(shape):
+    d, N, qw, qs, gen = SHAPES[shape]
+    _run(d, N, qw, qs, O.ADAM_AT_SERVER, T=6, gen=gen, split=True)
+
+
+def test_toy_full_trajectory():
+    """The toy quadratic at its full size, 100 steps, one-bucket scaled sign."""
+    w = W.WORKLOADS["toy"]
+    xs = W.toy_x_star(w)
+    pair = Pair(w.d, w.N, SIGN(0), SIGN(0), O.ADAM_AT_SERVER, seed=w.seed, x1=W.initial_x(w))
+    for t in range(1, w.steps + 1):
+        g = W.host_gradients(w, t, x=pair.ost.x, x_star=xs)   # from the oracle's iterate
+        pair.step(t, g)
+    pair.check_tie_budget()
+    print(f"\n[parity] toy: {pair.stats}", flush=True)
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["fused", "split"])
+@pytest.mark.parametrize("ex", ["ex1", "ex2"])
+def test_paper_toy_examples(ex, split):
+    """Examples 1 and 2 with Adam at the workers (Algorithms 1-2 as printed) on
+    the paper's 500-dimensional toy problem shape, 10 workers."""
+    t0 = W.PAPER_TOY
+    d, N = t0["d"], t0["N"]
+    q = qfields(O.Q_DET_UNIFORM, 2) if ex == "ex1" else qfields(O.Q_POW2, kmin=-17, kmax=-11)
+    rng = np.random.default_rng(3)
+    A = rng.standard_normal((d, d))
+    xs = rng.standard_normal(d) * np.sqrt(0.1)
+    pair = Pair(d, N, q, q, O.ADAM_AT_WORKER, seed=9, split=split, beta2=0.99, lr=1e-4)
+    for t in range(1, 41):
+        x = pair.ost.x.astype(np.float64)
+        xi = rng.standard_normal((N, d)) * np.sqrt(0.1)
+        pair.step(t, (2 * ((A @ x - xs)[None, :] - xi) @ A).astype(np.float32))
+    pair.check_tie_budget()
+
+
+KINDS = {
+    "none": qfields(O.Q_NONE),
+    "sign256": SIGN(256),
+    "sign_one": SIGN(0),
+    "stoch1_max": STOCH(1, O.SCALE_MAX, 256),
+    "stoch8_l2": STOCH(8, O.SCALE_L2, 512),
+    "stoch4_one": STOCH(4, O.SCALE_L2, 0),
+    "det3_512": qfields(O.Q_DET_UNIFORM, 3, bucket=512),
+    "det8_one": qfields(O.Q_DET_UNIFORM, 8),
+    "pow2_wide": qfields(O.Q_POW2, kmin=-20, kmax=-3),
+    "pow2_full": qfields(O.Q_POW2, kmin=-126, kmax=127),
+}
+
+
+@pytest.mark.parametrize("kind", list(KINDS))
+def test_quantizer_kinds(kind):
+    q = KINDS[kind]
+    _run(4 * 1024 + 260, 3, q, q, O.ADAM_AT_WORKER, T=5, gen="outliers")
+    _run(4 * 1024 + 260, 3, q, q, O.ADAM_AT_SERVER, T=5, gen="outliers")
+
+
+@pytest.mark.parametrize("ef", [(0, 0), (0, 1), (1, 0)], ids=["off-off", "off-on", "on-off"])
+def test_error_feedback_switches(ef):
+    _run(3000, 4, STOCH(2, O.SCALE_MAX, 512, ef[0]), SIGN(1024, ef[1]), O.ADAM_AT_SERVER, T=5)
+
+
+@pytest.mark.parametrize("d", [1, 3, 100, 255, 256, 257, 1001, 2049])
+def test_ragged_and_tiny_sizes(d):
+    """Sizes below one chunk, odd sizes (no 16-byte row alignment: scalar path)."""
+    _run(d, 3, STOCH(4, O.SCALE_L2, 256), SIGN(512), O.ADAM_AT_SERVER, T=4)
+    _run(d, 2, SIGN(0), STOCH(2, O.SCALE_MAX, 0), O.ADAM_AT_WORKER, T=4)
+
+
+def test_mixed_buckets_and_single_worker():
+    _run(5000, 1, STOCH(4, O.SCALE_L2, 2048), STOCH(2, O.SCALE_MAX, 256), O.ADAM_AT_SERVER, T=4)
+    _run(5000, 2, SIGN(256), SIGN(2048), O.ADAM_AT_WORKER, T=4)
+
+
+def test_zero_gradients_give_zero_scales():
+    d, N = 1300, 2
+    pair = Pair(d, N, STOCH(4, O.SCALE_L2, 256), qfields(O.Q_DET_UNIFORM, 2, bucket=512), O.ADAM_AT_SERVER,
+                eps=0.0)
+    g = np.zeros((N, d), np.float32)
+    g[:, 700:900] = 1e-3
+    for t in range(1, 4):
+        pair.step(t, g)
