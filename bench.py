@@ -67,6 +67,26 @@ def traffic_from_profile(workload: str, placement: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def stream_reference(rb, stream, reps=5):
+    """A plain in-place streaming op on the same buffers, timed the same way:
+    torch's e_w += g over N*d floats (two reads and one write per element),
+    the access mix closest to the round's.  Context for the roofline fraction;
+    it leaves e_w changed, so it runs after the timed rounds."""
+    import torch
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rb.e_w.add_(rb.g)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(reps):
+        rb.e_w.add_(rb.g)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / reps
+    nbytes = 12 * rb.g.numel()
+    return {"op": "torch e_w.add_(g), in place", "bytes": nbytes, "ms": round(ms, 4),
+            "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
 def cpu_baseline(E, w, cfg, rb, sample):
     """The oracle, as it stands, on the first `sample` parameters (one round)."""
     import numpy as np
@@ -171,6 +191,7 @@ def main():
         "hbm_frac": round(achieved / PEAK_HBM_GBS, 4),
         "roofline": roof,
     }
+    line["stream_reference"] = stream_reference(rb, stream)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(E, w, cfg, rb, args.cpu_sample)
     print(json.dumps(line), flush=True)

@@ -118,6 +118,8 @@ ea::QDev make_qdev(const ea_quant_t* q, int64_t d)
            : (q->kind == EA_Q_STOCH_UNIFORM && q->scale == EA_SCALE_L2) ? ea::S_L2 : ea::S_MAX;
     r.B = kind_has_scales(q->kind) ? bucket_len(q, d) : d;
     r.cpb = (kind_has_scales(q->kind) && !one_bucket(q, d)) ? (int32_t)(q->bucket / 256) : 0;
+    r.cpb_shift = 0;
+    while (r.cpb > 0 && (1 << r.cpb_shift) < r.cpb) ++r.cpb_shift;
     r.L = q->kind == EA_Q_STOCH_UNIFORM ? (1 << r.bits) - 1 : q->kind == EA_Q_DET_UNIFORM ? (1 << (r.bits - 1)) - 1 : 0;
     r.kmin = q->pow2_kmin;
     r.kmax = q->pow2_kmax;

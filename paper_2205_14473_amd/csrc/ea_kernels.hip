@@ -4,20 +4,51 @@
 // a block holds 4 independent waves.  Bucket norms are reduced inside the
 // wave (no LDS, no barrier); codes are bit-plane packed with one ballot per
 // 64-element plane word.  The fused step streams the N workers of a tile in
-// ascending worker order, keeps the dequantized sum in registers, and runs
-// the server's Adam, quantization and the parameter update on the same tile
-// (Algorithms 1-2, Section IV).
+// ascending worker order (the next worker's rows are loaded while the
+// current one is quantized), keeps the dequantized sum in registers, and
+// runs the server's Adam, quantization and the parameter update on the same
+// tile (Algorithms 1-2, Section IV).
+//
+// Every kernel is a template over the quantizer traits of both sides and the
+// Adam placement: QRt / placement -1 give the generic kernels used for any
+// configuration, QCt<...> the specialized ones for common shapes.  Tiles
+// that lie wholly inside d take a path without per-element bounds checks.
 #include "ea_launch.hpp"
 
 namespace ea {
 
 namespace {
 
-// Number of valid elements among lane's float4 at element n.
+// Largest number of waves in a block of the fused round (one worker each):
+// wide tiles need more registers per wave, so their blocks are narrower.
+#ifndef EA_WIDE_TILE_WAVES
+#define EA_WIDE_TILE_WAVES 8
+#endif
+#ifndef EA_ROUND_MIN_WAVES
+#define EA_ROUND_MIN_WAVES 6
+#endif
+__host__ __device__ constexpr int max_round_waves(int C)
+{
+    return C <= 2 ? 16 : (C == 4 ? 8 : EA_WIDE_TILE_WAVES);
+}
+
+// Minimum waves per SIMD the compiler must leave room for (caps VGPRs).
+__host__ __device__ constexpr int round_min_waves(int C)
+{
+    return C <= 2 ? EA_ROUND_MIN_WAVES : 1;
+}
+
+// Number of valid elements among a lane's float4 at element n.
 __device__ __forceinline__ int nvalid4(int64_t n, int64_t d)
 {
     const int64_t r = d - n;
     return r <= 0 ? 0 : (r >= 4 ? 4 : (int)r);
+}
+
+template <int PL>
+__device__ __forceinline__ int placement_of(const StepArgs& a)
+{
+    return PL < 0 ? a.placement : PL;
 }
 
 // ---------------------------------------------------------------------------
@@ -25,7 +56,7 @@ __device__ __forceinline__ int nvalid4(int64_t n, int64_t d)
 // a one-bucket quantizer), codes, bit-plane packing and the dequantized
 // values.  codes/scales point at the start of the message.
 // ---------------------------------------------------------------------------
-template <int C>
+template <int C, bool FULL, class QT>
 __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, const float4 (&p)[C],
                                               int64_t base, int nch, int64_t d, uint32_t k0, uint32_t k1,
                                               uint32_t step, uint32_t sid, float given_scale,
@@ -33,9 +64,16 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
                                               float4 (&deq)[C])
 {
     const int lane = lane_id();
+    const int kind = QT::kind(q);
+    const int norm = QT::norm(q);
+    const int cpb = QT::cpb(q);
+    const int bits = QT::bits(q);
+    if (FULL) nch = C;
+
+    const int64_t chunk0 = base >> 8;   // first chunk of the tile (tiles start on bucket boundaries)
     float s[C];
-    if (has_scale(q)) {
-        if (q.cpb == 0) {
+    if (has_scale<QT>(q)) {
+        if (cpb == 0) {
 #pragma unroll
             for (int ch = 0; ch < C; ++ch) s[ch] = given_scale;
         } else {
@@ -44,28 +82,29 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
             for (int ch = 0; ch < C; ++ch) {
                 part[ch].sum = 0.0;
                 part[ch].mx = 0.0f;
-                if (ch < nch) partial_add4(part[ch], q.norm, p[ch], nvalid4(base + ch * kChunk + 4 * lane, d));
+                if (ch < nch)
+                    partial_add4(part[ch], norm, p[ch], FULL ? 4 : nvalid4(base + ch * kChunk + 4 * lane, d));
             }
 #pragma unroll
             for (int ch = 0; ch < C; ++ch) {
-                if (ch % q.cpb == 0) {
+                if ((ch & (cpb - 1)) == 0) {
                     if (ch < nch) {
                         Partial tot;
                         tot.sum = 0.0;
                         tot.mx = 0.0f;
 #pragma unroll
                         for (int j = 0; j < C; ++j) {
-                            if (j >= ch && j < ch + q.cpb) {
+                            if (j >= ch && j < ch + cpb) {
                                 tot.sum += part[j].sum;
                                 tot.mx = fmaxf(tot.mx, part[j].mx);
                             }
                         }
                         const int64_t b0 = base + (int64_t)ch * kChunk;
-                        const int64_t nb = (d - b0) < q.B ? (d - b0) : q.B;
-                        const double S = q.norm == S_MAX ? 0.0 : wave_sum(tot.sum);
-                        const float M = q.norm == S_MAX ? wave_max(tot.mx) : 0.0f;
-                        s[ch] = scale_from(q.norm, S, M, nb);
-                        if (lane == 0) scales[b0 / q.B] = s[ch];
+                        const int64_t nb = FULL ? q.B : ((d - b0) < q.B ? (d - b0) : q.B);
+                        const double S = norm == S_MAX ? 0.0 : wave_sum(tot.sum);
+                        const float M = norm == S_MAX ? wave_max(tot.mx) : 0.0f;
+                        s[ch] = scale_from(norm, S, M, nb);
+                        if (lane == 0) st1(scales + ((chunk0 + ch) >> QT::cpb_shift(q)), s[ch]);
                     } else {
                         s[ch] = 0.0f;
                     }
@@ -79,16 +118,32 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
         for (int ch = 0; ch < C; ++ch) s[ch] = 1.0f;
     }
 
-    uint32_t c[C][4];
+    const bool gated = scale_gated<QT>(q);
+    if (kind == Q_NONE) {
+        float* raw = reinterpret_cast<float*>(codes);
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) {
+            deq[ch] = p[ch];
+            if (FULL || ch < nch) st4<false>(raw, base + (int64_t)ch * kChunk + 4 * lane, d, p[ch]);
+        }
+        return;
+    }
+    // Codes are produced slot by slot and each code plane goes straight into
+    // a ballot word, in message word order (4*chunk + slot)*bits + plane.
+    WordSink sink;
+    sink.out = codes + chunk0 * 4 * bits;
+    sink.lo = 0u;
+    sink.hi = 0u;
+    sink.filled = 0;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        const int nv = ch < nch ? nvalid4(n, d) : 0;
-        const float sc = s[ch];
-        const bool ok = sc > 0.0f && !isinf(sc);
-        const float inv = ok ? 1.0f / sc : 0.0f;
+        const int nv = FULL ? 4 : (ch < nch ? nvalid4(n, d) : 0);
+        const float sc = uniform(s[ch]);
+        const bool ok = !gated || (sc > 0.0f && !isinf(sc));
+        const float inv = 1.0f / (ok ? sc : 1.0f);
         uint4 r = make_uint4(0u, 0u, 0u, 0u);
-        if (q.kind == Q_STOCH && ch < nch) {
+        if (kind == Q_STOCH && (FULL || ch < nch)) {
             const uint64_t j = (uint64_t)n >> 2;
             r = philox10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), step, sid), k0, k1);
         }
@@ -96,32 +151,26 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const float x = comp(p[ch], k);
-            const bool valid = k < nv;
-            const uint32_t cc = valid ? code_of(q, x, inv, ok, u24(rr[k])) : 0u;
-            c[ch][k] = cc;
-            set_comp(deq[ch], k, valid ? deq_of(q, lut, cc, x, sc, ok) : 0.0f);
-        }
-    }
-
-    if (q.kind == Q_NONE) {
-        float* raw = reinterpret_cast<float*>(codes);
+            uint32_t cc = code_of<QT>(q, x, inv, rr[k]);
+            float dv = deq_of<QT>(q, lut, cc, x, sc);
+            if (gated && !ok) {
+                cc = zero_code_of<QT>(q);
+                dv = 0.0f;
+            }
+            if (!FULL && k >= nv) {
+                cc = 0u;
+                dv = 0.0f;
+            }
+            set_comp(deq[ch], k, dv);
+            if (FULL || ch < nch) {
+                if constexpr (QT::fixed) {
 #pragma unroll
-        for (int ch = 0; ch < C; ++ch)
-            if (ch < nch) st4<false>(raw, base + (int64_t)ch * kChunk + 4 * lane, d, p[ch]);
-        return;
-    }
-    WordSink sink;
-    sink.out = codes + (base / kChunk) * 4 * q.bits;
-    sink.lo = 0u;
-    sink.hi = 0u;
-    sink.filled = 0;
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (ch < nch) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                for (int pl = 0; pl < q.bits; ++pl)
-                    sink.put(__builtin_amdgcn_ballot_w64(((c[ch][k] >> pl) & 1u) != 0u));
+                    for (int pl = 0; pl < QT::bits(q); ++pl)
+                        sink.put(__builtin_amdgcn_ballot_w64(((cc >> pl) & 1u) != 0u));
+                } else {
+                    for (int pl = 0; pl < bits; ++pl)
+                        sink.put(__builtin_amdgcn_ballot_w64(((cc >> pl) & 1u) != 0u));
+                }
             }
         }
     }
@@ -129,97 +178,137 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
 }
 
 // Dequantize one tile of a message (the inverse of the code table).
-template <int C, bool VEC>
+template <int C, class QT>
 __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, const uint64_t* __restrict__ codes,
                                              const float* __restrict__ scales, int64_t base, int nch, int64_t d,
                                              float4 (&deq)[C])
 {
     const int lane = lane_id();
+    const int bits = QT::bits(q);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        deq[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        deq[ch] = zero4();
         if (ch >= nch) continue;
-        if (q.kind == Q_NONE) {
+        if (QT::kind(q) == Q_NONE) {
             deq[ch] = ld4<false>(reinterpret_cast<const float*>(codes), n, d);
             continue;
         }
-        const int64_t chunk = (base / kChunk) + ch;
+        const int64_t chunk = (base >> 8) + ch;
         float sc = 1.0f;
-        if (has_scale(q)) sc = scales[(chunk * kChunk) / q.B];
-        const bool ok = sc > 0.0f && !isinf(sc);
-        const uint64_t* w = codes + chunk * 4 * q.bits;
+        if (has_scale<QT>(q)) sc = scales[QT::cpb(q) == 0 ? 0 : (chunk >> QT::cpb_shift(q))];
+        sc = uniform(sc);
+        const bool ok = !scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc));
+        const uint64_t* w = codes + chunk * 4 * bits;
         const int nv = nvalid4(n, d);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             uint32_t cc = 0;
-            for (int pl = 0; pl < q.bits; ++pl) cc |= (uint32_t)((w[k * q.bits + pl] >> lane) & 1u) << pl;
-            set_comp(deq[ch], k, k < nv ? deq_of(q, lut, cc, 0.0f, sc, ok) : 0.0f);
+            for (int pl = 0; pl < bits; ++pl) cc |= (uint32_t)((w[k * bits + pl] >> lane) & 1u) << pl;
+            const float dv = ok ? deq_of<QT>(q, lut, cc, 0.0f, sc) : 0.0f;
+            set_comp(deq[ch], k, k < nv ? dv : 0.0f);
         }
     }
 }
 
-// p for worker rows: g + e (Adam at the server) or lr*m/sqrt(v) + e after the
-// moment update (Adam at the workers).  Moments are written back when asked.
-template <int C, bool VEC>
-__device__ __forceinline__ void worker_input(const StepArgs& a, const float* __restrict__ g,
-                                             const float* __restrict__ e, float* __restrict__ mw,
-                                             float* __restrict__ vw, int64_t base, int nch, bool store,
-                                             float4 (&p)[C])
+// Raw worker rows of one tile.
+template <int C>
+struct WorkerRows {
+    float4 g[C], e[C], m[C], v[C];
+};
+
+template <int C, bool VEC, bool FULL, int PL>
+__device__ __forceinline__ void load_worker(const StepArgs& a, const float* __restrict__ g,
+                                            const float* __restrict__ e, const float* __restrict__ mw,
+                                            const float* __restrict__ vw, int64_t base, int nch,
+                                            WorkerRows<C>& r)
 {
     const int lane = lane_id();
-    const float omb1 = 1.0f - a.beta1, omb2 = 1.0f - a.beta2;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        if (ch >= nch) {
-            p[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (!FULL && ch >= nch) {
+            r.g[ch] = r.e[ch] = r.m[ch] = r.v[ch] = zero4();
             continue;
         }
-        const float4 gv = ld4<VEC>(g, n, a.d);
-        const float4 ev = ld4<VEC>(e, n, a.d);
-        if (a.placement == AT_WORKER) {
-            float4 mv = ld4<VEC>(mw, n, a.d);
-            float4 vv = ld4<VEC>(vw, n, a.d);
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float gk = comp(gv, k);
-                const float vk = a.beta2 * comp(vv, k) + omb2 * (gk * gk);
-                const float mk = a.beta1 * comp(mv, k) + omb1 * gk;
-                set_comp(vv, k, vk);
-                set_comp(mv, k, mk);
-                const float uk = vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f;
-                set_comp(p[ch], k, uk + comp(ev, k));
-            }
-            if (store) {
-                st4<VEC>(mw, n, a.d, mv);
-                st4<VEC>(vw, n, a.d, vv);
-            }
-        } else {
-            p[ch] = make_float4(gv.x + ev.x, gv.y + ev.y, gv.z + ev.z, gv.w + ev.w);
+        r.g[ch] = ld4<VEC, FULL>(g, n, a.d);
+        r.e[ch] = ld4<VEC, FULL>(e, n, a.d);
+        if (placement_of<PL>(a) == AT_WORKER) {
+            r.m[ch] = ld4<VEC, FULL>(mw, n, a.d);
+            r.v[ch] = ld4<VEC, FULL>(vw, n, a.d);
         }
     }
 }
 
-// Server input from the worker average: Adam (at the server) or the average.
-template <int C, bool VEC>
+// p for a worker: g + e (Adam at the server) or lr*m/sqrt(v) + e after the
+// moment update (Adam at the workers); updated moments are left in r.
+template <int C, int PL>
+__device__ __forceinline__ void worker_p(const StepArgs& a, WorkerRows<C>& r, float4 (&p)[C])
+{
+    const float omb1 = 1.0f - a.beta1, omb2 = 1.0f - a.beta2;
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        if (placement_of<PL>(a) == AT_WORKER) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float gk = comp(r.g[ch], k);
+                const float vk = a.beta2 * comp(r.v[ch], k) + omb2 * (gk * gk);
+                const float mk = a.beta1 * comp(r.m[ch], k) + omb1 * gk;
+                set_comp(r.v[ch], k, vk);
+                set_comp(r.m[ch], k, mk);
+                const float uk = vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f;
+                set_comp(p[ch], k, uk + comp(r.e[ch], k));
+            }
+        } else {
+            p[ch] = add4(r.g[ch], r.e[ch]);
+        }
+    }
+}
+
+template <int C, bool VEC, bool FULL, int PL>
+__device__ __forceinline__ void store_moments(const StepArgs& a, float* __restrict__ mw, float* __restrict__ vw,
+                                              int64_t base, int nch, const WorkerRows<C>& r)
+{
+    if (placement_of<PL>(a) != AT_WORKER) return;
+    const int lane = lane_id();
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        if (!FULL && ch >= nch) continue;
+        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
+        st4<VEC, FULL>(mw, n, a.d, r.m[ch]);
+        st4<VEC, FULL>(vw, n, a.d, r.v[ch]);
+    }
+}
+
+// Average of the dequantized sum: a division by N, done as a multiplication
+// by 1/N when N is a power of two (both are the correctly rounded x/N).
+__device__ __forceinline__ float avg_of(float x, float fN, float invN, bool pow2)
+{
+    return pow2 ? x * invN : x / fN;
+}
+
+// Server input from the worker sum: Adam (at the server) or the average.
+template <int C, bool VEC, bool FULL, int PL>
 __device__ __forceinline__ void server_input(const StepArgs& a, const float4 (&acc)[C], int64_t base, int nch,
                                              float4 (&u)[C])
 {
     const int lane = lane_id();
     const float fN = (float)a.N;
+    const bool pow2 = (a.N & (a.N - 1)) == 0;
+    const float invN = 1.0f / fN;
     const float omb1 = 1.0f - a.beta1, omb2 = 1.0f - a.beta2;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        if (ch >= nch) {
-            u[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (!FULL && ch >= nch) {
+            u[ch] = zero4();
             continue;
         }
-        float4 avg = make_float4(acc[ch].x / fN, acc[ch].y / fN, acc[ch].z / fN, acc[ch].w / fN);
-        if (a.placement == AT_SERVER) {
-            float4 mv = ld4<VEC>(a.m, n, a.d);
-            float4 vv = ld4<VEC>(a.v, n, a.d);
+        float4 avg = make_float4(avg_of(acc[ch].x, fN, invN, pow2), avg_of(acc[ch].y, fN, invN, pow2),
+                                 avg_of(acc[ch].z, fN, invN, pow2), avg_of(acc[ch].w, fN, invN, pow2));
+        if (placement_of<PL>(a) == AT_SERVER) {
+            float4 mv = ld4<VEC, FULL>(a.m, n, a.d);
+            float4 vv = ld4<VEC, FULL>(a.v, n, a.d);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const float gk = comp(avg, k);
@@ -229,8 +318,8 @@ __device__ __forceinline__ void server_input(const StepArgs& a, const float4 (&a
                 set_comp(mv, k, mk);
                 set_comp(avg, k, vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f);
             }
-            st4<VEC>(a.m, n, a.d, mv);
-            st4<VEC>(a.v, n, a.d, vv);
+            st4<VEC, FULL>(a.m, n, a.d, mv);
+            st4<VEC, FULL>(a.v, n, a.d, vv);
         }
         u[ch] = avg;
     }
@@ -266,97 +355,177 @@ __device__ __forceinline__ bool tile_pos(const StepArgs& a, TilePos& t)
     return true;
 }
 
-// ---------------------------------------------------------------------------
-// Kernels
-// ---------------------------------------------------------------------------
-
-// The fused round.  With a one-bucket Q_w the worker scales are read from
-// wscales (computed beforehand); with a one-bucket Q_s the kernel stops after
-// the server input, which it leaves in ubuf with per-tile partial norms.
-template <int C, bool VEC>
-__global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a)
+template <int C>
+__device__ __forceinline__ bool tile_full(const StepArgs& a, const TilePos& t)
 {
-    __shared__ float lut_w[kLutSize];
-    __shared__ float lut_s[kLutSize];
-    fill_lut(a.qw, lut_w);
-    fill_lut(a.qs, lut_s);
-    __syncthreads();
-    TilePos t;
-    if (!tile_pos<C>(a, t)) return;
+    return t.base + (int64_t)C * kChunk <= a.d;
+}
+
+// ---------------------------------------------------------------------------
+// The fused round, one tile per block.  The block has G = min(N, 16) waves.
+// Workers are taken in groups of G: wave w quantizes worker g0 + w of the
+// tile and hands its dequantized values to wave 0 through LDS; wave 0 adds
+// them in ascending worker order (the order of the average in Algorithm 1)
+// and, after the last group, runs the server side on the tile.  Short-lived
+// per-worker waves keep far more independent memory traffic in flight than
+// one wave looping over all workers.  The handoff buffer is double-buffered,
+// so one barrier per group suffices: a buffer is rewritten only after the
+// barrier that wave 0 reaches once it has read the buffer's previous group.
+// ---------------------------------------------------------------------------
+template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
+__device__ __forceinline__ void round_tile(const StepArgs& a, const TilePos& t, const float* lut_w,
+                                           const float* lut_s, float4* xfer, int G)
+{
     const int lane = lane_id();
-    const bool wglobal = has_scale(a.qw) && a.qw.cpb == 0;
-    const bool sglobal = has_scale(a.qs) && a.qs.cpb == 0;
+    const int w = (int)(threadIdx.x / kWave);
+    const bool wglobal = has_scale<QW>(a.qw) && QW::cpb(a.qw) == 0;
+    const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
+    const bool atw = placement_of<PL>(a) == AT_WORKER;
 
     float4 acc[C];
 #pragma unroll
-    for (int ch = 0; ch < C; ++ch) acc[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
 
-    for (int i = 0; i < a.N; ++i) {
-        const int64_t row = (int64_t)i * a.d;
-        float* e = a.e_w + row;
-        float4 p[C], dq[C];
-        worker_input<C, VEC>(a, a.g + row, e, a.m_w ? a.m_w + row : nullptr, a.v_w ? a.v_w + row : nullptr,
-                             t.base, t.nch, true, p);
-        const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
-        quantize_tile<C>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
-                         a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales, dq);
+    int buf = 0;
+    for (int g0 = 0; g0 < a.N; g0 += G, buf ^= 1) {
+        float4* slot = xfer + ((int64_t)buf * G * C) * kWave;
+        const int i = g0 + w;
+        if (i < a.N) {
+            const int64_t row = (int64_t)i * a.d;
+            WorkerRows<C> r;
+            load_worker<C, VEC, FULL, PL>(a, a.g + row, a.e_w + row, atw ? a.m_w + row : nullptr,
+                                          atw ? a.v_w + row : nullptr, t.base, t.nch, r);
+            float4 p[C], dq[C];
+            worker_p<C, PL>(a, r, p);
+            if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
+            const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
+            quantize_tile<C, FULL, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
+                                       a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales,
+                                       dq);
+            float* e = a.e_w + row;
 #pragma unroll
-        for (int ch = 0; ch < C; ++ch) {
-            if (ch >= t.nch) continue;
-            const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-            float4 r = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            if (a.qw.ef) r = make_float4(p[ch].x - dq[ch].x, p[ch].y - dq[ch].y, p[ch].z - dq[ch].z, p[ch].w - dq[ch].w);
-            st4<VEC>(e, n, a.d, r);
-            acc[ch] = make_float4(acc[ch].x + dq[ch].x, acc[ch].y + dq[ch].y, acc[ch].z + dq[ch].z,
-                                  acc[ch].w + dq[ch].w);
+            for (int ch = 0; ch < C; ++ch) {
+                if (!FULL && ch >= t.nch) continue;
+                const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
+                st4<VEC, FULL>(e, n, a.d, a.qw.ef ? sub4(p[ch], dq[ch]) : zero4());
+            }
+#pragma unroll
+            for (int ch = 0; ch < C; ++ch) slot[(w * C + ch) * kWave + lane] = dq[ch];
+        }
+        __syncthreads();
+        if (w == 0) {
+            const int cnt = a.N - g0 < G ? a.N - g0 : G;
+            for (int j = 0; j < cnt; ++j) {
+#pragma unroll
+                for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], slot[(j * C + ch) * kWave + lane]);
+            }
         }
     }
+    if (w != 0) return;
 
     float4 u[C], q[C], dq[C];
-    server_input<C, VEC>(a, acc, t.base, t.nch, u);
+    server_input<C, VEC, FULL, PL>(a, acc, t.base, t.nch, u);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
-        if (ch >= t.nch) {
-            q[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (!FULL && ch >= t.nch) {
+            q[ch] = zero4();
             continue;
         }
-        const float4 es = ld4<VEC>(a.e_s, t.base + (int64_t)ch * kChunk + 4 * lane, a.d);
-        q[ch] = make_float4(u[ch].x + es.x, u[ch].y + es.y, u[ch].z + es.z, u[ch].w + es.w);
+        q[ch] = add4(u[ch], ld4<VEC, FULL>(a.e_s, t.base + (int64_t)ch * kChunk + 4 * lane, a.d));
     }
     if (sglobal) {
 #pragma unroll
         for (int ch = 0; ch < C; ++ch)
-            if (ch < t.nch) st4<VEC>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
+            if (FULL || ch < t.nch) st4<VEC, FULL>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
         const double part = tile_partial<C>(a.qs, q, t.base, t.nch, a.d);
         if (lane == 0) a.spart[t.tile] = part;
         return;
     }
-    quantize_tile<C>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, 0.0f, a.scodes,
-                     a.sscales, dq);
+    quantize_tile<C, FULL, QS>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, 0.0f, a.scodes,
+                               a.sscales, dq);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
-        if (ch >= t.nch) continue;
+        if (!FULL && ch >= t.nch) continue;
         const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        float4 r = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (a.qs.ef) r = make_float4(q[ch].x - dq[ch].x, q[ch].y - dq[ch].y, q[ch].z - dq[ch].z, q[ch].w - dq[ch].w);
-        st4<VEC>(a.e_s, n, a.d, r);
-        const float4 xv = ld4<VEC>(a.x, n, a.d);
-        st4<VEC>(a.x, n, a.d, make_float4(xv.x - dq[ch].x, xv.y - dq[ch].y, xv.z - dq[ch].z, xv.w - dq[ch].w));
+        st4<VEC, FULL>(a.e_s, n, a.d, a.qs.ef ? sub4(q[ch], dq[ch]) : zero4());
+        st4<VEC, FULL>(a.x, n, a.d, sub4(ld4<VEC, FULL>(a.x, n, a.d), dq[ch]));
     }
 }
 
+// ---------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------
+
+// Dynamic LDS of a fused-round block with G waves: the two code tables plus
+// the handoff of G workers' tiles (double-buffered when N > G).
+inline size_t round_lds_bytes(int N, int C, int G)
+{
+    const int nbuf = N > G ? 2 : 1;
+    return 2 * kLutSize * sizeof(float) + (size_t)nbuf * G * C * kWave * sizeof(float4);
+}
+
+// Waves per block: one per worker up to the tile's limit, fewer if the LDS
+// would exceed what a block may use.
+inline int round_waves(int N, int C, size_t lds_limit)
+{
+    int G = N < max_round_waves(C) ? N : max_round_waves(C);
+    while (G > 1 && round_lds_bytes(N, C, G) > lds_limit) G = (G + 1) / 2;
+    return G;
+}
+
+// Per-block LDS limit of the current device (queried once per device).
+size_t lds_limit_bytes()
+{
+    static size_t cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 64 * 1024;
+    if (cached[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
+            v = 64 * 1024;
+        cached[dev] = (size_t)v;
+    }
+    return cached[dev];
+}
+
+// The fused round.  With a one-bucket Q_w the worker scales are read from
+// wscales (computed beforehand); with a one-bucket Q_s the block stops after
+// the server input, which it leaves in ubuf with per-tile partial norms.
+template <int C, bool VEC, class QW, class QS, int PL>
+__global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C)) void step_kernel(StepArgs a)
+{
+    extern __shared__ float4 smem[];
+    float* lut_w = reinterpret_cast<float*>(smem);
+    float* lut_s = lut_w + kLutSize;
+    float4* xfer = smem + (2 * kLutSize) / 4;
+    fill_lut(a.qw, lut_w);
+    fill_lut(a.qs, lut_s);
+    __syncthreads();
+    TilePos t;
+    t.tile = blockIdx.x;
+    t.base = t.tile * C * kChunk;
+    const int64_t rem = (a.d - t.base + kChunk - 1) / kChunk;
+    t.nch = rem < C ? (int)rem : C;
+    const int G = (int)(blockDim.x / kWave);
+    if (VEC && tile_full<C>(a, t)) round_tile<C, VEC, true, QW, QS, PL>(a, t, lut_w, lut_s, xfer, G);
+    else round_tile<C, VEC, false, QW, QS, PL>(a, t, lut_w, lut_s, xfer, G);
+}
+
 // Per-tile partial norms of the worker inputs p for workers [i0, i1), without
-// writing any state (one-bucket Q_w).  Rows are [i][d] from a.g / a.e_w.
+// writing any state (one-bucket Q_w).  Rows are [i - i0][d] from a.g etc.
 template <int C, bool VEC>
 __global__ __launch_bounds__(kBlock) void worker_partials_kernel(StepArgs a, int i0, int i1)
 {
     TilePos t;
     if (!tile_pos<C>(a, t)) return;
+    const bool atw = a.placement == AT_WORKER;
     for (int i = i0; i < i1; ++i) {
         const int64_t row = (int64_t)(i - i0) * a.d;
+        WorkerRows<C> r;
         float4 p[C];
-        worker_input<C, VEC>(a, a.g + row, a.e_w + row, a.m_w ? a.m_w + row : nullptr,
-                             a.v_w ? a.v_w + row : nullptr, t.base, t.nch, false, p);
+        load_worker<C, VEC, false, -1>(a, a.g + row, a.e_w + row, atw ? a.m_w + row : nullptr,
+                                       atw ? a.v_w + row : nullptr, t.base, t.nch, r);
+        worker_p<C, -1>(a, r, p);
         const double part = tile_partial<C>(a.qw, p, t.base, t.nch, a.d);
         if (lane_id() == 0) a.wpart[(int64_t)(i - i0) * a.ntiles + t.tile] = part;
     }
@@ -372,12 +541,10 @@ __global__ __launch_bounds__(kBlock) void server_partials_kernel(StepArgs a)
     float4 q[C];
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
-        q[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        q[ch] = zero4();
         if (ch >= t.nch) continue;
         const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        const float4 uv = ld4<VEC>(a.ubuf, n, a.d);
-        const float4 es = ld4<VEC>(a.e_s, n, a.d);
-        q[ch] = make_float4(uv.x + es.x, uv.y + es.y, uv.z + es.z, uv.w + es.w);
+        q[ch] = add4(ld4<VEC>(a.ubuf, n, a.d), ld4<VEC>(a.e_s, n, a.d));
     }
     const double part = tile_partial<C>(a.qs, q, t.base, t.nch, a.d);
     if (lane == 0) a.spart[t.tile] = part;
@@ -420,18 +587,20 @@ __global__ __launch_bounds__(kBlock) void worker_kernel(StepArgs a)
     TilePos t;
     if (!tile_pos<C>(a, t)) return;
     const int lane = lane_id();
-    const bool wglobal = has_scale(a.qw) && a.qw.cpb == 0;
+    const bool wglobal = has_scale<QRt>(a.qw) && a.qw.cpb == 0;
+    const bool atw = a.placement == AT_WORKER;
+    WorkerRows<C> r;
     float4 p[C], dq[C];
-    worker_input<C, VEC>(a, a.g, a.e_w, a.m_w, a.v_w, t.base, t.nch, true, p);
+    load_worker<C, VEC, false, -1>(a, a.g, a.e_w, a.m_w, a.v_w, t.base, t.nch, r);
+    worker_p<C, -1>(a, r, p);
+    if (atw) store_moments<C, VEC, false, -1>(a, a.m_w, a.v_w, t.base, t.nch, r);
     const float gs = wglobal ? a.wscales[0] : 0.0f;
-    quantize_tile<C>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)a.worker, gs, a.wcodes,
-                     a.wscales, dq);
+    quantize_tile<C, false, QRt>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)a.worker, gs,
+                                 a.wcodes, a.wscales, dq);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         if (ch >= t.nch) continue;
-        float4 r = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (a.qw.ef) r = make_float4(p[ch].x - dq[ch].x, p[ch].y - dq[ch].y, p[ch].z - dq[ch].z, p[ch].w - dq[ch].w);
-        st4<VEC>(a.e_w, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, r);
+        st4<VEC>(a.e_w, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, a.qw.ef ? sub4(p[ch], dq[ch]) : zero4());
     }
 }
 
@@ -448,16 +617,14 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
     const int lane = lane_id();
     float4 acc[C], dq[C], u[C];
 #pragma unroll
-    for (int ch = 0; ch < C; ++ch) acc[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
     for (int i = 0; i < a.N; ++i) {
-        dequant_tile<C, VEC>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
-                             a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, dq);
+        dequant_tile<C, QRt>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales,
+                             t.base, t.nch, a.d, dq);
 #pragma unroll
-        for (int ch = 0; ch < C; ++ch)
-            acc[ch] = make_float4(acc[ch].x + dq[ch].x, acc[ch].y + dq[ch].y, acc[ch].z + dq[ch].z,
-                                  acc[ch].w + dq[ch].w);
+        for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
     }
-    server_input<C, VEC>(a, acc, t.base, t.nch, u);
+    server_input<C, VEC, false, -1>(a, acc, t.base, t.nch, u);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch)
         if (ch < t.nch) st4<VEC>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
@@ -473,31 +640,24 @@ __global__ __launch_bounds__(kBlock) void server_kernel(StepArgs a)
     TilePos t;
     if (!tile_pos<C>(a, t)) return;
     const int lane = lane_id();
-    const bool sglobal = has_scale(a.qs) && a.qs.cpb == 0;
+    const bool sglobal = has_scale<QRt>(a.qs) && a.qs.cpb == 0;
     float4 q[C], dq[C];
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
-        q[ch] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        q[ch] = zero4();
         if (ch >= t.nch) continue;
         const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        const float4 uv = ld4<VEC>(a.ubuf, n, a.d);
-        const float4 es = ld4<VEC>(a.e_s, n, a.d);
-        q[ch] = make_float4(uv.x + es.x, uv.y + es.y, uv.z + es.z, uv.w + es.w);
+        q[ch] = add4(ld4<VEC>(a.ubuf, n, a.d), ld4<VEC>(a.e_s, n, a.d));
     }
     const float gs = sglobal ? a.sscales[0] : 0.0f;
-    quantize_tile<C>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, gs, a.scodes,
-                     a.sscales, dq);
+    quantize_tile<C, false, QRt>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, gs, a.scodes,
+                                 a.sscales, dq);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         if (ch >= t.nch) continue;
         const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        float4 r = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (a.qs.ef) r = make_float4(q[ch].x - dq[ch].x, q[ch].y - dq[ch].y, q[ch].z - dq[ch].z, q[ch].w - dq[ch].w);
-        st4<VEC>(a.e_s, n, a.d, r);
-        if (a.apply) {
-            const float4 xv = ld4<VEC>(a.x, n, a.d);
-            st4<VEC>(a.x, n, a.d, make_float4(xv.x - dq[ch].x, xv.y - dq[ch].y, xv.z - dq[ch].z, xv.w - dq[ch].w));
-        }
+        st4<VEC>(a.e_s, n, a.d, a.qs.ef ? sub4(q[ch], dq[ch]) : zero4());
+        if (a.apply) st4<VEC>(a.x, n, a.d, sub4(ld4<VEC>(a.x, n, a.d), dq[ch]));
     }
 }
 
@@ -512,13 +672,12 @@ __global__ __launch_bounds__(kBlock) void apply_kernel(StepArgs a)
     if (!tile_pos<C>(a, t)) return;
     const int lane = lane_id();
     float4 dq[C];
-    dequant_tile<C, VEC>(a.qs, lut_s, a.scodes, a.sscales, t.base, t.nch, a.d, dq);
+    dequant_tile<C, QRt>(a.qs, lut_s, a.scodes, a.sscales, t.base, t.nch, a.d, dq);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         if (ch >= t.nch) continue;
         const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        const float4 xv = ld4<VEC>(a.x, n, a.d);
-        st4<VEC>(a.x, n, a.d, make_float4(xv.x - dq[ch].x, xv.y - dq[ch].y, xv.z - dq[ch].z, xv.w - dq[ch].w));
+        st4<VEC>(a.x, n, a.d, sub4(ld4<VEC>(a.x, n, a.d), dq[ch]));
     }
 }
 
@@ -533,7 +692,7 @@ int64_t grid_of(const StepArgs& a)
     return (a.ntiles + kWavesPerBlock - 1) / kWavesPerBlock;
 }
 
-// Dispatch on (C, VEC) to a kernel template instance.
+// Dispatch on (C, VEC) to a generic kernel template instance.
 #define EA_DISPATCH(KERNEL, C, VEC, GRID, STREAM, ...)                                              \
     do {                                                                                           \
         switch ((C) * 2 + ((VEC) ? 1 : 0)) {                                                       \
@@ -549,12 +708,82 @@ int64_t grid_of(const StepArgs& a)
         }                                                                                          \
     } while (0)
 
+// Specialized fused rounds: (chunks per tile, worker traits, server traits,
+// placement), chosen when the configuration matches exactly and rows are
+// 16-byte aligned.
+using SignQ8 = QCt<Q_SCALED_SIGN, 1, S_L1, 8>;
+using SignQ4 = QCt<Q_SCALED_SIGN, 1, S_L1, 4>;
+using SignQ2 = QCt<Q_SCALED_SIGN, 1, S_L1, 2>;
+using Stoch4L2Q2 = QCt<Q_STOCH, 4, S_L2, 2>;
+using Stoch2MaxQ2 = QCt<Q_STOCH, 2, S_MAX, 2>;
+using Stoch2MaxQ4 = QCt<Q_STOCH, 2, S_MAX, 4>;
+
+struct Special {
+    int C;
+    int wkind, wbits, wnorm, wcpb;
+    int skind, sbits, snorm, scpb;
+    int placement;
+    void (*kernel)(StepArgs);
+};
+
+#define EA_SPECIAL(CC, QWT, QST, PLC)                                                               \
+    Special{CC, QWT::kind(QDev{}), QWT::bits(QDev{}), QWT::norm(QDev{}), QWT::cpb(QDev{}),         \
+            QST::kind(QDev{}), QST::bits(QDev{}), QST::norm(QDev{}), QST::cpb(QDev{}), PLC,         \
+            step_kernel<CC, true, QWT, QST, PLC>}
+
+const Special kSpecials[] = {
+    EA_SPECIAL(2, Stoch4L2Q2, Stoch4L2Q2, AT_SERVER),
+    EA_SPECIAL(2, Stoch4L2Q2, Stoch4L2Q2, AT_WORKER),
+    EA_SPECIAL(2, Stoch2MaxQ2, Stoch2MaxQ2, AT_SERVER),
+    EA_SPECIAL(2, Stoch2MaxQ2, Stoch2MaxQ2, AT_WORKER),
+    EA_SPECIAL(8, SignQ8, SignQ8, AT_SERVER),
+    EA_SPECIAL(8, SignQ8, SignQ8, AT_WORKER),
+    EA_SPECIAL(4, Stoch2MaxQ4, SignQ4, AT_SERVER),
+    EA_SPECIAL(4, Stoch2MaxQ4, SignQ4, AT_WORKER),
+    EA_SPECIAL(2, SignQ2, SignQ2, AT_SERVER),
+};
+
+const Special* find_special(const StepArgs& a, int C)
+{
+    for (const Special& s : kSpecials) {
+        if (s.C == C && s.placement == a.placement && s.wkind == a.qw.kind && s.wbits == a.qw.bits &&
+            s.wnorm == a.qw.norm && s.wcpb == a.qw.cpb && s.skind == a.qs.kind && s.sbits == a.qs.bits &&
+            s.snorm == a.qs.norm && s.scpb == a.qs.cpb)
+            return &s;
+    }
+    return nullptr;
+}
+
 }  // namespace
 
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
-    EA_DISPATCH(step_kernel, C, vec, grid_of(a), s, a);
+    const size_t limit = lds_limit_bytes();
+    const int G = round_waves(a.N, C, limit);
+    const dim3 grid((unsigned)a.ntiles), block((unsigned)(G * kWave));
+    const size_t lds = round_lds_bytes(a.N, C, G);
+    const Special* sp = vec ? find_special(a, C) : nullptr;
+    if (sp) {
+        hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, a);
+        return hipGetLastError();
+    }
+    switch (C * 2 + (vec ? 1 : 0)) {
+    case 2: hipLaunchKernelGGL((step_kernel<1, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    case 3: hipLaunchKernelGGL((step_kernel<1, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    case 4: hipLaunchKernelGGL((step_kernel<2, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    case 5: hipLaunchKernelGGL((step_kernel<2, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    case 8: hipLaunchKernelGGL((step_kernel<4, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    case 9: hipLaunchKernelGGL((step_kernel<4, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    case 16: hipLaunchKernelGGL((step_kernel<8, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    case 17: hipLaunchKernelGGL((step_kernel<8, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
+}
+
+bool has_special_step(const StepArgs& a, int C, bool vec)
+{
+    return vec && find_special(a, C) != nullptr;
 }
 
 hipError_t launch_worker_partials(const StepArgs& a, int C, bool vec, int i0, int i1, hipStream_t s)

@@ -44,6 +44,8 @@ struct StepArgs {
 
 // Launchers; C = chunks per tile (1..8), vec = rows are 16-byte aligned.
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s);
+// True when launch_step uses a kernel specialized for this configuration.
+bool has_special_step(const StepArgs& a, int C, bool vec);
 hipError_t launch_worker_partials(const StepArgs& a, int C, bool vec, int i0, int i1, hipStream_t s);
 hipError_t launch_server_partials(const StepArgs& a, int C, bool vec, hipStream_t s);
 hipError_t launch_finalize(const double* part, int64_t ntiles, int32_t norm, int64_t n, float* out,
