@@ -55,16 +55,22 @@ def algorithmic_bytes(E, cfg) -> int:
 
 
 def traffic_from_profile(workload: str, placement: str):
-    """HBM bytes per launch measured by rocprofv3 counters, if the committed
-    counter summary was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", f"step_kernel_{workload}_{placement}_pmc.json")
+    """HBM bytes per launch measured by rocprofv3 counters (FETCH_SIZE and
+    WRITE_SIZE, each scaled by what it reads for a plain copy of known size),
+    if the committed counter summary was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"step_kernel_{workload}_{placement}_pmc.txt")
     if not os.path.exists(path):
         return None
+    rec = {}
     with open(path) as f:
-        rec = json.load(f)
+        for line in f:
+            if line.startswith("#") or ":" not in line:
+                continue
+            k, v = line.split(":", 1)
+            rec[k.strip()] = v.strip()
     if rec.get("source_digest") != source_digest():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return int(rec["hbm_bytes_per_launch"])
 
 
 def stream_reference(rb, stream, reps=5):
