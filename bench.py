@@ -8,9 +8,11 @@ bucket scale, bucket 512, two-way error feedback) unless --workload says
 otherwise.  Inputs are synthetic (workloads.py) and already in HBM when the
 timed region starts; the N gradient buffers are generated once and reused.
 
-Prints ONE JSON line.  `roofline` covers the dominant kernel (step_kernel,
-the only kernel of a bucketed round): achieved = algorithmic HBM bytes per
-round / mean round time from HIP events on the launch stream.
+Prints ONE JSON line.  `roofline` covers step_kernel, the only kernel of a
+bucketed round (one launch over the tiles that lie wholly inside d, plus a
+one-block launch for the ragged last tile when d is not a multiple of the
+tile): achieved = algorithmic HBM bytes per round / mean round time from HIP
+events on the launch stream, i.e. over both launches.
 `cpu_baseline` times the oracle (single-threaded C) on a bounded sample.
 """
 import argparse
@@ -55,9 +57,10 @@ def algorithmic_bytes(E, cfg) -> int:
 
 
 def traffic_from_profile(workload: str, placement: str):
-    """HBM bytes per launch measured by rocprofv3 counters (FETCH_SIZE and
-    WRITE_SIZE, each scaled by what it reads for a plain copy of known size),
-    if the committed counter summary was taken on the current kernel sources."""
+    """HBM bytes per round measured by rocprofv3 counters (FETCH_SIZE and
+    WRITE_SIZE summed over the round's step_kernel launches, each scaled by
+    what it reads for a plain copy of known size), if the committed counter
+    summary was taken on the current kernel sources."""
     path = os.path.join(ROOT, "profiles", f"step_kernel_{workload}_{placement}_pmc.txt")
     if not os.path.exists(path):
         return None
@@ -70,7 +73,7 @@ def traffic_from_profile(workload: str, placement: str):
             rec[k.strip()] = v.strip()
     if rec.get("source_digest") != source_digest():
         return None
-    return int(rec["hbm_bytes_per_launch"])
+    return int(rec["hbm_bytes_per_round"])
 
 
 def stream_reference(rb, stream, reps=5):
@@ -184,7 +187,7 @@ def main():
     value = cfg.d / (ms * 1e-3) / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(args.workload, args.placement),
-            "kernel": "step_kernel", "algorithmic_bytes_per_launch": alg,
+            "kernel": "step_kernel (whole tiles + ragged tail)", "algorithmic_bytes_per_round": alg,
             "bytes_per_param": round(alg / cfg.d, 2)}
     line = {
         "metric": METRIC, "value": round(value, 4), "unit": "Gparam/s", "n_gpus": 1, "steps": args.steps,

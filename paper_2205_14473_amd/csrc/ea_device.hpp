@@ -22,6 +22,11 @@ constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kLutSize = 512;        // largest code table (POW2 with 9-bit codes)
 constexpr uint32_t kServerStream = 0xFFFFFFFFu;
 
+__device__ __forceinline__ int lane_id()
+{
+    return (int)(threadIdx.x & (kWave - 1));
+}
+
 enum : int32_t { Q_NONE = 0, Q_SCALED_SIGN = 1, Q_STOCH = 2, Q_DET = 3, Q_POW2 = 4 };
 enum : int32_t { S_L1 = 0, S_L2 = 1, S_MAX = 2 };
 enum : int32_t { AT_SERVER = 0, AT_WORKER = 1 };
@@ -226,9 +231,10 @@ __device__ __forceinline__ float scale_from(int norm, double sum, float mx, int6
 // Code tables.  value = scale * lut[code] for SCALED_SIGN / STOCH / DET,
 // value = lut[code] for POW2.
 // ---------------------------------------------------------------------------
+template <class QT>
 __device__ __forceinline__ float lut_entry(const QDev& q, int32_t c)
 {
-    switch (q.kind) {
+    switch (QT::kind(q)) {
     case Q_SCALED_SIGN:
         return c == 0 ? 1.0f : -1.0f;
     case Q_STOCH:
@@ -236,20 +242,43 @@ __device__ __forceinline__ float lut_entry(const QDev& q, int32_t c)
     case Q_DET:
         return c <= 2 * q.L ? (float)(c - q.L) / (float)q.L : 0.0f;
     case Q_POW2: {
-        if (c >= (1 << q.bits)) return 0.0f;
-        const int32_t mag = c & ((1 << (q.bits - 1)) - 1);
+        const int bits = QT::bits(q);
+        if (c >= (1 << bits)) return 0.0f;
+        const int32_t mag = c & ((1 << (bits - 1)) - 1);
         if (mag > q.kmax - q.kmin) return 0.0f;          // the zero code (and unused codes)
         const float v = __uint_as_float((uint32_t)(mag + q.kmin + 127) << 23);
-        return (c >> (q.bits - 1)) ? -v : v;
+        return (c >> (bits - 1)) ? -v : v;
     }
     default:
         return 0.0f;
     }
 }
 
+// Whole-block table (any code width); the caller synchronizes the block.
 __device__ __forceinline__ void fill_lut(const QDev& q, float* lut)
 {
-    for (int c = threadIdx.x; c < kLutSize; c += blockDim.x) lut[c] = lut_entry(q, c);
+    for (int c = threadIdx.x; c < kLutSize; c += blockDim.x) lut[c] = lut_entry<QRt>(q, c);
+}
+
+// Tables of specialized quantizers with codes below 64 are built per wave:
+// lane l writes entry l of its own wave's table, and only that wave reads it,
+// so no block barrier is needed.
+template <class QT>
+struct WaveTable {
+    static constexpr bool value = false;
+};
+template <int K, int B, int NM, int CPB>
+struct WaveTable<QCt<K, B, NM, CPB>> {
+    static constexpr bool value = B <= 6;
+};
+
+template <class QT>
+__device__ __forceinline__ void fill_wave_table(const QDev& q, float* tab)
+{
+    tab[lane_id()] = lut_entry<QT>(q, lane_id());
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // ---------------------------------------------------------------------------
@@ -268,15 +297,15 @@ __device__ __forceinline__ uint32_t code_of(const QDev& q, float p, float inv, u
         // clamp to [0, L]; y never reaches L with a positive fraction, so
         // lo + 1 never exceeds L.
         const float y = __builtin_amdgcn_fmed3f((p * inv + 1.0f) * (Lf * 0.5f), 0.0f, Lf);
-        const float lo = floorf(y);
-        return (uint32_t)lo + (u24(r) < y - lo ? 1u : 0u);
+        // y >= 0: truncation is the floor, and y - floor(y) is exact.
+        return (uint32_t)y + (u24(r) < __builtin_amdgcn_fractf(y) ? 1u : 0u);
     }
     case Q_DET: {
         const float Lf = (float)q.L;
         float a = fabsf(p) * inv * Lf;
         a = a > Lf ? Lf : a;
-        int32_t i = (int32_t)floorf(a);
-        if (a - (float)i > 0.5f) i += 1;
+        int32_t i = (int32_t)a;                            // a >= 0: the floor
+        if (__builtin_amdgcn_fractf(a) > 0.5f) i += 1;
         return (uint32_t)((p < 0.0f ? -i : i) + q.L);
     }
     case Q_POW2: {
@@ -426,11 +455,6 @@ __device__ __forceinline__ float4 sub4(float4 a, float4 b)
 __device__ __forceinline__ float4 zero4()
 {
     return make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-}
-
-__device__ __forceinline__ int lane_id()
-{
-    return (int)(threadIdx.x & (kWave - 1));
 }
 
 // v_writelane_b32: write a wave-uniform 32-bit value into one lane of a VGPR.

@@ -24,18 +24,27 @@ namespace {
 #ifndef EA_WIDE_TILE_WAVES
 #define EA_WIDE_TILE_WAVES 8
 #endif
+#ifndef EA_NARROW_TILE_WAVES
+#define EA_NARROW_TILE_WAVES 16
+#endif
 #ifndef EA_ROUND_MIN_WAVES
 #define EA_ROUND_MIN_WAVES 6
 #endif
+#ifndef EA_EDGE_MIN_WAVES
+#define EA_EDGE_MIN_WAVES 5
+#endif
 __host__ __device__ constexpr int max_round_waves(int C)
 {
-    return C <= 2 ? 16 : (C == 4 ? 8 : EA_WIDE_TILE_WAVES);
+    return C <= 2 ? EA_NARROW_TILE_WAVES : (C == 4 ? 8 : EA_WIDE_TILE_WAVES);
 }
 
 // Minimum waves per SIMD the compiler must leave room for (caps VGPRs).
-__host__ __device__ constexpr int round_min_waves(int C)
+// Kernels over whole tiles with Adam at the server have no per-element
+// bounds checks and no worker moments, and need fewer registers than the
+// others.
+__host__ __device__ constexpr int round_min_waves(int C, bool lean)
 {
-    return C <= 2 ? EA_ROUND_MIN_WAVES : 1;
+    return C <= 2 ? (lean ? EA_ROUND_MIN_WAVES : EA_EDGE_MIN_WAVES) : 1;
 }
 
 // Number of valid elements among a lane's float4 at element n.
@@ -135,13 +144,34 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
     sink.lo = 0u;
     sink.hi = 0u;
     sink.filled = 0;
+    // The scale, its reciprocal and the gate are wave-uniform and computed
+    // once per bucket.
+    float sc = 0.0f, inv = 0.0f;
+    bool ok = true;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
         const int nv = FULL ? 4 : (ch < nch ? nvalid4(n, d) : 0);
-        const float sc = uniform(s[ch]);
-        const bool ok = !gated || (sc > 0.0f && !isinf(sc));
-        const float inv = 1.0f / (ok ? sc : 1.0f);
+        if (ch == 0 || (cpb != 0 && (ch & (cpb - 1)) == 0)) {
+            sc = uniform(s[ch]);
+            ok = !gated || (sc > 0.0f && !isinf(sc));
+            inv = 1.0f / sc;
+        }
+        if (!ok) {
+            // Zero or non-finite scale (uniform over the wave): the chunk is
+            // sent as zero codes and dequantizes to zero.
+            const uint32_t zc = zero_code_of<QT>(q);
+            deq[ch] = zero4();
+            if (FULL || ch < nch) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const bool valid = FULL || k < nv;
+                    for (int pl = 0; pl < bits; ++pl)
+                        sink.put(__builtin_amdgcn_ballot_w64(valid && ((zc >> pl) & 1u) != 0u));
+                }
+            }
+            continue;
+        }
         uint4 r = make_uint4(0u, 0u, 0u, 0u);
         if (kind == Q_STOCH && (FULL || ch < nch)) {
             const uint64_t j = (uint64_t)n >> 2;
@@ -153,10 +183,6 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
             const float x = comp(p[ch], k);
             uint32_t cc = code_of<QT>(q, x, inv, rr[k]);
             float dv = deq_of<QT>(q, lut, cc, x, sc);
-            if (gated && !ok) {
-                cc = zero_code_of<QT>(q);
-                dv = 0.0f;
-            }
             if (!FULL && k >= nv) {
                 cc = 0u;
                 dv = 0.0f;
@@ -164,9 +190,11 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
             set_comp(deq[ch], k, dv);
             if (FULL || ch < nch) {
                 if constexpr (QT::fixed) {
+                    // Codes are below 2^bits, so the top plane is a compare.
 #pragma unroll
                     for (int pl = 0; pl < QT::bits(q); ++pl)
-                        sink.put(__builtin_amdgcn_ballot_w64(((cc >> pl) & 1u) != 0u));
+                        sink.put(__builtin_amdgcn_ballot_w64(pl == QT::bits(q) - 1 ? cc >= (1u << pl)
+                                                                                    : ((cc >> pl) & 1u) != 0u));
                 } else {
                     for (int pl = 0; pl < bits; ++pl)
                         sink.put(__builtin_amdgcn_ballot_w64(((cc >> pl) & 1u) != 0u));
@@ -280,6 +308,32 @@ __device__ __forceinline__ void store_moments(const StepArgs& a, float* __restri
     }
 }
 
+// The server's rows of one tile: Adam moments (Adam at the server), the
+// server error and x.
+template <int C>
+struct ServerRows {
+    float4 m[C], v[C], e[C], x[C];
+};
+
+template <int C, bool VEC, bool FULL, int PL>
+__device__ __forceinline__ void load_server(const StepArgs& a, int64_t base, int nch, bool with_e, bool with_x,
+                                            ServerRows<C>& r)
+{
+    const int lane = lane_id();
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
+        r.m[ch] = r.v[ch] = r.e[ch] = r.x[ch] = zero4();
+        if (!FULL && ch >= nch) continue;
+        if (placement_of<PL>(a) == AT_SERVER) {
+            r.m[ch] = ld4<VEC, FULL>(a.m, n, a.d);
+            r.v[ch] = ld4<VEC, FULL>(a.v, n, a.d);
+        }
+        if (with_e) r.e[ch] = ld4<VEC, FULL>(a.e_s, n, a.d);
+        if (with_x) r.x[ch] = ld4<VEC, FULL>(a.x, n, a.d);
+    }
+}
+
 // Average of the dequantized sum: a division by N, done as a multiplication
 // by 1/N when N is a power of two (both are the correctly rounded x/N).
 __device__ __forceinline__ float avg_of(float x, float fN, float invN, bool pow2)
@@ -290,7 +344,7 @@ __device__ __forceinline__ float avg_of(float x, float fN, float invN, bool pow2
 // Server input from the worker sum: Adam (at the server) or the average.
 template <int C, bool VEC, bool FULL, int PL>
 __device__ __forceinline__ void server_input(const StepArgs& a, const float4 (&acc)[C], int64_t base, int nch,
-                                             float4 (&u)[C])
+                                             ServerRows<C>& sr, float4 (&u)[C])
 {
     const int lane = lane_id();
     const float fN = (float)a.N;
@@ -307,8 +361,8 @@ __device__ __forceinline__ void server_input(const StepArgs& a, const float4 (&a
         float4 avg = make_float4(avg_of(acc[ch].x, fN, invN, pow2), avg_of(acc[ch].y, fN, invN, pow2),
                                  avg_of(acc[ch].z, fN, invN, pow2), avg_of(acc[ch].w, fN, invN, pow2));
         if (placement_of<PL>(a) == AT_SERVER) {
-            float4 mv = ld4<VEC, FULL>(a.m, n, a.d);
-            float4 vv = ld4<VEC, FULL>(a.v, n, a.d);
+            float4 mv = sr.m[ch];
+            float4 vv = sr.v[ch];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const float gk = comp(avg, k);
@@ -355,10 +409,52 @@ __device__ __forceinline__ bool tile_pos(const StepArgs& a, TilePos& t)
     return true;
 }
 
-template <int C>
-__device__ __forceinline__ bool tile_full(const StepArgs& a, const TilePos& t)
+// ---------------------------------------------------------------------------
+// One worker's share of a tile: wave w compresses worker i and leaves its
+// dequantized values in the handoff slot.
+template <int C, bool VEC, bool FULL, int PL>
+__device__ __forceinline__ void worker_load(const StepArgs& a, const TilePos& t, int i, WorkerRows<C>& r)
 {
-    return t.base + (int64_t)C * kChunk <= a.d;
+    const bool atw = placement_of<PL>(a) == AT_WORKER;
+    const int64_t row = (int64_t)i * a.d;
+    load_worker<C, VEC, FULL, PL>(a, a.g + row, a.e_w + row, atw ? a.m_w + row : nullptr,
+                                  atw ? a.v_w + row : nullptr, t.base, t.nch, r);
+}
+
+template <int C, bool VEC, bool FULL, class QW, int PL>
+__device__ __forceinline__ void worker_compute(const StepArgs& a, const TilePos& t, const float* lut_w, int i,
+                                               WorkerRows<C>& r, float4* slot)
+{
+    const int lane = lane_id();
+    const bool wglobal = has_scale<QW>(a.qw) && QW::cpb(a.qw) == 0;
+    const bool atw = placement_of<PL>(a) == AT_WORKER;
+    const int64_t row = (int64_t)i * a.d;
+    float4 p[C], dq[C];
+    worker_p<C, PL>(a, r, p);
+    if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
+    const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
+    quantize_tile<C, FULL, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
+                               a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales, dq);
+    float* e = a.e_w + row;
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        if (!FULL && ch >= t.nch) continue;
+        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
+        st4<VEC, FULL>(e, n, a.d, a.qw.ef ? sub4(p[ch], dq[ch]) : zero4());
+    }
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) slot[ch * kWave + lane] = dq[ch];
+}
+
+// Wave 0: add the cnt handoff slots of a group, in ascending worker order.
+template <int C>
+__device__ __forceinline__ void gather_group(const float4* slot, int cnt, float4 (&acc)[C])
+{
+    const int lane = lane_id();
+    for (int j = 0; j < cnt; ++j) {
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], slot[(j * C + ch) * kWave + lane]);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -371,6 +467,9 @@ __device__ __forceinline__ bool tile_full(const StepArgs& a, const TilePos& t)
 // one wave looping over all workers.  The handoff buffer is double-buffered,
 // so one barrier per group suffices: a buffer is rewritten only after the
 // barrier that wave 0 reaches once it has read the buffer's previous group.
+// The last group is peeled off so that wave 0 can issue the server's loads
+// before the last barrier: their latency overlaps the wait for the other
+// workers, without the loaded rows being live during the earlier groups.
 // ---------------------------------------------------------------------------
 template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
 __device__ __forceinline__ void round_tile(const StepArgs& a, const TilePos& t, const float* lut_w,
@@ -378,61 +477,38 @@ __device__ __forceinline__ void round_tile(const StepArgs& a, const TilePos& t, 
 {
     const int lane = lane_id();
     const int w = (int)(threadIdx.x / kWave);
-    const bool wglobal = has_scale<QW>(a.qw) && QW::cpb(a.qw) == 0;
     const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
-    const bool atw = placement_of<PL>(a) == AT_WORKER;
 
     float4 acc[C];
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
 
-    int buf = 0;
-    for (int g0 = 0; g0 < a.N; g0 += G, buf ^= 1) {
+    // Wave w takes workers w, w + G, ...
+    int buf = 0, g0 = 0;
+    for (; g0 + G < a.N; g0 += G, buf ^= 1) {
         float4* slot = xfer + ((int64_t)buf * G * C) * kWave;
-        const int i = g0 + w;
-        if (i < a.N) {
-            const int64_t row = (int64_t)i * a.d;
-            WorkerRows<C> r;
-            load_worker<C, VEC, FULL, PL>(a, a.g + row, a.e_w + row, atw ? a.m_w + row : nullptr,
-                                          atw ? a.v_w + row : nullptr, t.base, t.nch, r);
-            float4 p[C], dq[C];
-            worker_p<C, PL>(a, r, p);
-            if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
-            const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
-            quantize_tile<C, FULL, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
-                                       a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales,
-                                       dq);
-            float* e = a.e_w + row;
-#pragma unroll
-            for (int ch = 0; ch < C; ++ch) {
-                if (!FULL && ch >= t.nch) continue;
-                const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-                st4<VEC, FULL>(e, n, a.d, a.qw.ef ? sub4(p[ch], dq[ch]) : zero4());
-            }
-#pragma unroll
-            for (int ch = 0; ch < C; ++ch) slot[(w * C + ch) * kWave + lane] = dq[ch];
-        }
+        WorkerRows<C> r;
+        worker_load<C, VEC, FULL, PL>(a, t, g0 + w, r);
+        worker_compute<C, VEC, FULL, QW, PL>(a, t, lut_w, g0 + w, r, slot + w * C * kWave);
         __syncthreads();
-        if (w == 0) {
-            const int cnt = a.N - g0 < G ? a.N - g0 : G;
-            for (int j = 0; j < cnt; ++j) {
-#pragma unroll
-                for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], slot[(j * C + ch) * kWave + lane]);
-            }
-        }
+        if (w == 0) gather_group<C>(slot, G, acc);
     }
+    float4* slot = xfer + ((int64_t)buf * G * C) * kWave;
+    if (g0 + w < a.N) {
+        WorkerRows<C> r;
+        worker_load<C, VEC, FULL, PL>(a, t, g0 + w, r);
+        worker_compute<C, VEC, FULL, QW, PL>(a, t, lut_w, g0 + w, r, slot + w * C * kWave);
+    }
+    ServerRows<C> sr;
+    if (w == 0) load_server<C, VEC, FULL, PL>(a, t.base, t.nch, true, !sglobal, sr);
+    __syncthreads();
     if (w != 0) return;
+    gather_group<C>(slot, a.N - g0, acc);
 
     float4 u[C], q[C], dq[C];
-    server_input<C, VEC, FULL, PL>(a, acc, t.base, t.nch, u);
+    server_input<C, VEC, FULL, PL>(a, acc, t.base, t.nch, sr, u);
 #pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (!FULL && ch >= t.nch) {
-            q[ch] = zero4();
-            continue;
-        }
-        q[ch] = add4(u[ch], ld4<VEC, FULL>(a.e_s, t.base + (int64_t)ch * kChunk + 4 * lane, a.d));
-    }
+    for (int ch = 0; ch < C; ++ch) q[ch] = add4(u[ch], sr.e[ch]);
     if (sglobal) {
 #pragma unroll
         for (int ch = 0; ch < C; ++ch)
@@ -448,7 +524,7 @@ __device__ __forceinline__ void round_tile(const StepArgs& a, const TilePos& t, 
         if (!FULL && ch >= t.nch) continue;
         const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
         st4<VEC, FULL>(a.e_s, n, a.d, a.qs.ef ? sub4(q[ch], dq[ch]) : zero4());
-        st4<VEC, FULL>(a.x, n, a.d, sub4(ld4<VEC, FULL>(a.x, n, a.d), dq[ch]));
+        st4<VEC, FULL>(a.x, n, a.d, sub4(sr.x[ch], dq[ch]));
     }
 }
 
@@ -456,12 +532,19 @@ __device__ __forceinline__ void round_tile(const StepArgs& a, const TilePos& t, 
 // Kernels
 // ---------------------------------------------------------------------------
 
-// Dynamic LDS of a fused-round block with G waves: the two code tables plus
-// the handoff of G workers' tiles (double-buffered when N > G).
+// Floats of the code-table region of a fused-round block with G waves: room
+// for both block-wide tables or for two 64-entry tables per wave.
+__host__ __device__ constexpr int table_floats(int G)
+{
+    return 2 * kLutSize > 2 * kWave * G ? 2 * kLutSize : 2 * kWave * G;
+}
+
+// Dynamic LDS of a fused-round block with G waves: the code tables plus the
+// handoff of G workers' tiles (double-buffered when N > G).
 inline size_t round_lds_bytes(int N, int C, int G)
 {
     const int nbuf = N > G ? 2 : 1;
-    return 2 * kLutSize * sizeof(float) + (size_t)nbuf * G * C * kWave * sizeof(float4);
+    return table_floats(G) * sizeof(float) + (size_t)nbuf * G * C * kWave * sizeof(float4);
 }
 
 // Waves per block: one per worker up to the tile's limit, fewer if the LDS
@@ -491,24 +574,39 @@ size_t lds_limit_bytes()
 // The fused round.  With a one-bucket Q_w the worker scales are read from
 // wscales (computed beforehand); with a one-bucket Q_s the block stops after
 // the server input, which it leaves in ubuf with per-tile partial norms.
-template <int C, bool VEC, class QW, class QS, int PL>
-__global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C)) void step_kernel(StepArgs a)
+//
+// FULL kernels (rows 16-byte aligned) take the tiles that lie wholly inside d
+// and carry no bounds checks; the others take any tile.  Block b works on
+// tile a.tile0 + b.
+template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
+__global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
+    StepArgs a)
 {
+    static_assert(!FULL || VEC, "whole-tile kernels need aligned rows");
     extern __shared__ float4 smem[];
-    float* lut_w = reinterpret_cast<float*>(smem);
-    float* lut_s = lut_w + kLutSize;
-    float4* xfer = smem + (2 * kLutSize) / 4;
-    fill_lut(a.qw, lut_w);
-    fill_lut(a.qs, lut_s);
-    __syncthreads();
+    const int G = (int)(blockDim.x / kWave);
+    float* lut_w;
+    float* lut_s;
+    if constexpr (WaveTable<QW>::value && WaveTable<QS>::value) {
+        float* tab = reinterpret_cast<float*>(smem) + (threadIdx.x / kWave) * 2 * kWave;
+        fill_wave_table<QW>(a.qw, tab);
+        fill_wave_table<QS>(a.qs, tab + kWave);
+        lut_w = tab;
+        lut_s = tab + kWave;
+    } else {
+        lut_w = reinterpret_cast<float*>(smem);
+        lut_s = lut_w + kLutSize;
+        fill_lut(a.qw, lut_w);
+        fill_lut(a.qs, lut_s);
+        __syncthreads();
+    }
+    float4* xfer = smem + table_floats(G) / 4;
     TilePos t;
-    t.tile = blockIdx.x;
+    t.tile = a.tile0 + blockIdx.x;
     t.base = t.tile * C * kChunk;
     const int64_t rem = (a.d - t.base + kChunk - 1) / kChunk;
     t.nch = rem < C ? (int)rem : C;
-    const int G = (int)(blockDim.x / kWave);
-    if (VEC && tile_full<C>(a, t)) round_tile<C, VEC, true, QW, QS, PL>(a, t, lut_w, lut_s, xfer, G);
-    else round_tile<C, VEC, false, QW, QS, PL>(a, t, lut_w, lut_s, xfer, G);
+    round_tile<C, VEC, FULL, QW, QS, PL>(a, t, lut_w, lut_s, xfer, G);
 }
 
 // Per-tile partial norms of the worker inputs p for workers [i0, i1), without
@@ -624,7 +722,9 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
 #pragma unroll
         for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
     }
-    server_input<C, VEC, false, -1>(a, acc, t.base, t.nch, u);
+    ServerRows<C> sr;
+    load_server<C, VEC, false, -1>(a, t.base, t.nch, false, false, sr);
+    server_input<C, VEC, false, -1>(a, acc, t.base, t.nch, sr, u);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch)
         if (ch < t.nch) st4<VEC>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
@@ -729,7 +829,7 @@ struct Special {
 #define EA_SPECIAL(CC, QWT, QST, PLC)                                                               \
     Special{CC, QWT::kind(QDev{}), QWT::bits(QDev{}), QWT::norm(QDev{}), QWT::cpb(QDev{}),         \
             QST::kind(QDev{}), QST::bits(QDev{}), QST::norm(QDev{}), QST::cpb(QDev{}), PLC,         \
-            step_kernel<CC, true, QWT, QST, PLC>}
+            step_kernel<CC, true, true, QWT, QST, PLC>}
 
 const Special kSpecials[] = {
     EA_SPECIAL(2, Stoch4L2Q2, Stoch4L2Q2, AT_SERVER),
@@ -756,29 +856,49 @@ const Special* find_special(const StepArgs& a, int C)
 
 }  // namespace
 
+// Whole tiles go to a kernel without bounds checks (specialized when one
+// matches the configuration); the ragged last tile, and every tile of rows
+// that are not 16-byte aligned, go to the generic checked kernel.
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
     const size_t limit = lds_limit_bytes();
     const int G = round_waves(a.N, C, limit);
-    const dim3 grid((unsigned)a.ntiles), block((unsigned)(G * kWave));
+    const dim3 block((unsigned)(G * kWave));
     const size_t lds = round_lds_bytes(a.N, C, G);
-    const Special* sp = vec ? find_special(a, C) : nullptr;
-    if (sp) {
-        hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, a);
+    const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) : 0;
+    if (nfull > 0) {
+        StepArgs b = a;
+        b.tile0 = 0;
+        const dim3 grid((unsigned)nfull);
+        const Special* sp = find_special(a, C);
+        if (sp) {
+            hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
+        } else {
+            switch (C) {
+            case 1: hipLaunchKernelGGL((step_kernel<1, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 2: hipLaunchKernelGGL((step_kernel<2, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 4: hipLaunchKernelGGL((step_kernel<4, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 8: hipLaunchKernelGGL((step_kernel<8, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            default: return hipErrorInvalidValue;
+            }
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (nfull < a.ntiles) {
+        StepArgs b = a;
+        b.tile0 = nfull;
+        const dim3 grid((unsigned)(a.ntiles - nfull));
+        switch (C) {
+        case 1: hipLaunchKernelGGL((step_kernel<1, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        case 2: hipLaunchKernelGGL((step_kernel<2, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        case 4: hipLaunchKernelGGL((step_kernel<4, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        case 8: hipLaunchKernelGGL((step_kernel<8, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        default: return hipErrorInvalidValue;
+        }
         return hipGetLastError();
     }
-    switch (C * 2 + (vec ? 1 : 0)) {
-    case 2: hipLaunchKernelGGL((step_kernel<1, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    case 3: hipLaunchKernelGGL((step_kernel<1, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    case 4: hipLaunchKernelGGL((step_kernel<2, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    case 5: hipLaunchKernelGGL((step_kernel<2, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    case 8: hipLaunchKernelGGL((step_kernel<4, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    case 9: hipLaunchKernelGGL((step_kernel<4, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    case 16: hipLaunchKernelGGL((step_kernel<8, false, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    case 17: hipLaunchKernelGGL((step_kernel<8, true, QRt, QRt, -1>), grid, block, lds, s, a); break;
-    default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 bool has_special_step(const StepArgs& a, int C, bool vec)
