@@ -28,7 +28,7 @@ namespace {
 #define EA_NARROW_TILE_WAVES 16
 #endif
 #ifndef EA_ROUND_MIN_WAVES
-#define EA_ROUND_MIN_WAVES 6
+#define EA_ROUND_MIN_WAVES 5
 #endif
 #ifndef EA_EDGE_MIN_WAVES
 #define EA_EDGE_MIN_WAVES 5
@@ -38,13 +38,30 @@ __host__ __device__ constexpr int max_round_waves(int C)
     return C <= 2 ? EA_NARROW_TILE_WAVES : (C == 4 ? 8 : EA_WIDE_TILE_WAVES);
 }
 
+// Tiles per block of the fused round.  Lean kernels (whole tiles, Adam at
+// the server) take two consecutive tiles per block; the others one.
+#ifndef EA_TILES_PER_BLOCK
+#define EA_TILES_PER_BLOCK 2
+#endif
+__host__ __device__ constexpr int round_tiles_per_block(int C, bool lean)
+{
+    return C <= 2 && lean ? EA_TILES_PER_BLOCK : 1;
+}
+
 // Minimum waves per SIMD the compiler must leave room for (caps VGPRs).
 // Kernels over whole tiles with Adam at the server have no per-element
 // bounds checks and no worker moments, and need fewer registers than the
 // others.
+#ifndef EA_C4_MIN_WAVES
+#define EA_C4_MIN_WAVES 1
+#endif
+#ifndef EA_C8_MIN_WAVES
+#define EA_C8_MIN_WAVES 3
+#endif
 __host__ __device__ constexpr int round_min_waves(int C, bool lean)
 {
-    return C <= 2 ? (lean ? EA_ROUND_MIN_WAVES : EA_EDGE_MIN_WAVES) : 1;
+    return C <= 2 ? (lean ? EA_ROUND_MIN_WAVES : EA_EDGE_MIN_WAVES)
+                  : (lean ? (C == 4 ? EA_C4_MIN_WAVES : EA_C8_MIN_WAVES) : 1);
 }
 
 // Number of valid elements among a lane's float4 at element n.
@@ -63,14 +80,28 @@ __device__ __forceinline__ int placement_of(const StepArgs& a)
 // ---------------------------------------------------------------------------
 // Quantize one tile: scales (reduced per bucket inside the wave, or given for
 // a one-bucket quantizer), codes, bit-plane packing and the dequantized
-// values.  codes/scales point at the start of the message.
+// values.  codes/scales point at the start of the message.  The code words go
+// to `sink`, which the caller opens at the tile's first word (message_sink)
+// and flushes; consecutive tiles may share one sink, since their words are
+// consecutive in the message.
 // ---------------------------------------------------------------------------
+template <class QT>
+__device__ __forceinline__ WordSink message_sink(const QDev& q, uint64_t* codes, int64_t base)
+{
+    WordSink sink;
+    sink.out = codes + (base >> 8) * 4 * QT::bits(q);
+    sink.lo = 0u;
+    sink.hi = 0u;
+    sink.filled = 0;
+    return sink;
+}
+
 template <int C, bool FULL, class QT>
 __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, const float4 (&p)[C],
                                               int64_t base, int nch, int64_t d, uint32_t k0, uint32_t k1,
                                               uint32_t step, uint32_t sid, float given_scale,
                                               uint64_t* __restrict__ codes, float* __restrict__ scales,
-                                              float4 (&deq)[C])
+                                              WordSink& sink, float4 (&deq)[C])
 {
     const int lane = lane_id();
     const int kind = QT::kind(q);
@@ -113,7 +144,10 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
                         const double S = norm == S_MAX ? 0.0 : wave_sum(tot.sum);
                         const float M = norm == S_MAX ? wave_max(tot.mx) : 0.0f;
                         s[ch] = scale_from(norm, S, M, nb);
-                        if (lane == 0) st1(scales + ((chunk0 + ch) >> QT::cpb_shift(q)), s[ch]);
+                        // A plain store: the caches merge the 4-byte scales of
+                        // neighbouring tiles, where streaming stores reach HBM
+                        // one partial line at a time.
+                        if (lane == 0) scales[(chunk0 + ch) >> QT::cpb_shift(q)] = s[ch];
                     } else {
                         s[ch] = 0.0f;
                     }
@@ -139,11 +173,6 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
     }
     // Codes are produced slot by slot and each code plane goes straight into
     // a ballot word, in message word order (4*chunk + slot)*bits + plane.
-    WordSink sink;
-    sink.out = codes + chunk0 * 4 * bits;
-    sink.lo = 0u;
-    sink.hi = 0u;
-    sink.filled = 0;
     // The scale, its reciprocal and the gate are wave-uniform and computed
     // once per bucket.
     float sc = 0.0f, inv = 0.0f;
@@ -202,7 +231,6 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
             }
         }
     }
-    sink.flush();
 }
 
 // Dequantize one tile of a message (the inverse of the code table).
@@ -423,7 +451,7 @@ __device__ __forceinline__ void worker_load(const StepArgs& a, const TilePos& t,
 
 template <int C, bool VEC, bool FULL, class QW, int PL>
 __device__ __forceinline__ void worker_compute(const StepArgs& a, const TilePos& t, const float* lut_w, int i,
-                                               WorkerRows<C>& r, float4* slot)
+                                               WorkerRows<C>& r, WordSink& sink, float4* slot)
 {
     const int lane = lane_id();
     const bool wglobal = has_scale<QW>(a.qw) && QW::cpb(a.qw) == 0;
@@ -434,7 +462,7 @@ __device__ __forceinline__ void worker_compute(const StepArgs& a, const TilePos&
     if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
     const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
     quantize_tile<C, FULL, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
-                               a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales, dq);
+                               a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales, sink, dq);
     float* e = a.e_w + row;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
@@ -457,53 +485,89 @@ __device__ __forceinline__ void gather_group(const float4* slot, int cnt, float4
     }
 }
 
+// Position of tile `tile` of C chunks.
+template <int C>
+__device__ __forceinline__ TilePos tile_at(const StepArgs& a, int64_t tile)
+{
+    TilePos t;
+    t.tile = tile;
+    t.base = tile * C * kChunk;
+    const int64_t rem = (a.d - t.base + kChunk - 1) / kChunk;
+    t.nch = rem < C ? (int)rem : C;
+    return t;
+}
+
+// Worker i on the block's nt consecutive tiles: the rows of all of them are
+// loaded first, so the later tiles' loads are in flight while the first is
+// compressed; the codes of the tiles leave through one sink, as one piece.
+// Tile k's dequantized values go to slots + (k*G + w)*C*64.
+template <int C, int K, bool VEC, bool FULL, class QW, int PL>
+__device__ __forceinline__ void worker_tiles(const StepArgs& a, const TilePos (&tp)[K], int nt, const float* lut_w,
+                                             int i, float4* slots, int G, int w)
+{
+    WorkerRows<C> r[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+        if (k < nt) worker_load<C, VEC, FULL, PL>(a, tp[k], i, r[k]);
+    WordSink sink = message_sink<QW>(a.qw, a.wcodes + (int64_t)i * a.qw.words, tp[0].base);
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+        if (k < nt)
+            worker_compute<C, VEC, FULL, QW, PL>(a, tp[k], lut_w, i, r[k], sink,
+                                                 slots + ((int64_t)k * G + w) * C * kWave);
+    sink.flush();
+}
+
 // ---------------------------------------------------------------------------
-// The fused round, one tile per block.  The block has G = min(N, 16) waves.
-// Workers are taken in groups of G: wave w quantizes worker g0 + w of the
-// tile and hands its dequantized values to wave 0 through LDS; wave 0 adds
-// them in ascending worker order (the order of the average in Algorithm 1)
-// and, after the last group, runs the server side on the tile.  Short-lived
-// per-worker waves keep far more independent memory traffic in flight than
-// one wave looping over all workers.  The handoff buffer is double-buffered,
-// so one barrier per group suffices: a buffer is rewritten only after the
-// barrier that wave 0 reaches once it has read the buffer's previous group.
-// The last group is peeled off so that wave 0 can issue the server's loads
-// before the last barrier: their latency overlaps the wait for the other
-// workers, without the loaded rows being live during the earlier groups.
+// The fused round on nt <= K consecutive tiles per block.  The block has
+// G = min(N, 16) waves.  Workers are taken in groups of G: wave w compresses
+// worker g0 + w on every tile of the block and hands its dequantized values
+// over through LDS.  Wave k then serves tile k: it adds the handoffs in
+// ascending worker order (the order of the average in Algorithm 1) and, after
+// the last group, runs the server side on its tile.  Short-lived per-worker
+// waves keep far more independent memory traffic in flight than one wave
+// looping over all workers, and serving the tiles on separate waves keeps the
+// server work off the workers' path.  The handoff is double-buffered over
+// groups, so one barrier per group suffices: a buffer is rewritten only after
+// the barrier that the serving waves reach once they have read the buffer's
+// previous group.  The last group is peeled off so that the serving waves can
+// issue the server's loads before the last barrier: their latency overlaps
+// the wait for the workers, without the loaded rows being live during the
+// earlier groups.
 // ---------------------------------------------------------------------------
-template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
-__device__ __forceinline__ void round_tile(const StepArgs& a, const TilePos& t, const float* lut_w,
-                                           const float* lut_s, float4* xfer, int G)
+template <int C, int K, bool VEC, bool FULL, class QW, class QS, int PL>
+__device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, int nt, const float* lut_w,
+                                            const float* lut_s, float4* xfer, int G)
 {
     const int lane = lane_id();
     const int w = (int)(threadIdx.x / kWave);
     const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
 
+    TilePos tp[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) tp[k] = tile_at<C>(a, tile0 + k);
+
     float4 acc[C];
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
 
-    // Wave w takes workers w, w + G, ...
+    // Handoff layout: [group buffer][tile][wave][chunk][lane].
+    const int64_t per_buf = (int64_t)K * G * C * kWave;
     int buf = 0, g0 = 0;
     for (; g0 + G < a.N; g0 += G, buf ^= 1) {
-        float4* slot = xfer + ((int64_t)buf * G * C) * kWave;
-        WorkerRows<C> r;
-        worker_load<C, VEC, FULL, PL>(a, t, g0 + w, r);
-        worker_compute<C, VEC, FULL, QW, PL>(a, t, lut_w, g0 + w, r, slot + w * C * kWave);
+        float4* slots = xfer + buf * per_buf;
+        worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
         __syncthreads();
-        if (w == 0) gather_group<C>(slot, G, acc);
+        if (w < nt) gather_group<C>(slots + (int64_t)w * G * C * kWave, G, acc);
     }
-    float4* slot = xfer + ((int64_t)buf * G * C) * kWave;
-    if (g0 + w < a.N) {
-        WorkerRows<C> r;
-        worker_load<C, VEC, FULL, PL>(a, t, g0 + w, r);
-        worker_compute<C, VEC, FULL, QW, PL>(a, t, lut_w, g0 + w, r, slot + w * C * kWave);
-    }
+    float4* slots = xfer + buf * per_buf;
+    if (g0 + w < a.N) worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
+    const TilePos t = tile_at<C>(a, tile0 + (w < nt ? w : 0));
     ServerRows<C> sr;
-    if (w == 0) load_server<C, VEC, FULL, PL>(a, t.base, t.nch, true, !sglobal, sr);
+    if (w < nt) load_server<C, VEC, FULL, PL>(a, t.base, t.nch, true, !sglobal, sr);
     __syncthreads();
-    if (w != 0) return;
-    gather_group<C>(slot, a.N - g0, acc);
+    if (w >= nt) return;
+    gather_group<C>(slots + (int64_t)w * G * C * kWave, a.N - g0, acc);
 
     float4 u[C], q[C], dq[C];
     server_input<C, VEC, FULL, PL>(a, acc, t.base, t.nch, sr, u);
@@ -517,8 +581,10 @@ __device__ __forceinline__ void round_tile(const StepArgs& a, const TilePos& t, 
         if (lane == 0) a.spart[t.tile] = part;
         return;
     }
+    WordSink sink = message_sink<QS>(a.qs, a.scodes, t.base);
     quantize_tile<C, FULL, QS>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, 0.0f, a.scodes,
-                               a.sscales, dq);
+                               a.sscales, sink, dq);
+    sink.flush();
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         if (!FULL && ch >= t.nch) continue;
@@ -541,18 +607,18 @@ __host__ __device__ constexpr int table_floats(int G)
 
 // Dynamic LDS of a fused-round block with G waves: the code tables plus the
 // handoff of G workers' tiles (double-buffered when N > G).
-inline size_t round_lds_bytes(int N, int C, int G)
+inline size_t round_lds_bytes(int N, int C, int G, int K)
 {
     const int nbuf = N > G ? 2 : 1;
-    return table_floats(G) * sizeof(float) + (size_t)nbuf * G * C * kWave * sizeof(float4);
+    return table_floats(G) * sizeof(float) + (size_t)nbuf * K * G * C * kWave * sizeof(float4);
 }
 
 // Waves per block: one per worker up to the tile's limit, fewer if the LDS
 // would exceed what a block may use.
-inline int round_waves(int N, int C, size_t lds_limit)
+inline int round_waves(int N, int C, int K, size_t lds_limit)
 {
     int G = N < max_round_waves(C) ? N : max_round_waves(C);
-    while (G > 1 && round_lds_bytes(N, C, G) > lds_limit) G = (G + 1) / 2;
+    while (G > 1 && round_lds_bytes(N, C, G, K) > lds_limit) G = (G + 1) / 2;
     return G;
 }
 
@@ -576,8 +642,9 @@ size_t lds_limit_bytes()
 // the server input, which it leaves in ubuf with per-tile partial norms.
 //
 // FULL kernels (rows 16-byte aligned) take the tiles that lie wholly inside d
-// and carry no bounds checks; the others take any tile.  Block b works on
-// tile a.tile0 + b.
+// and carry no bounds checks; the others take any tile.  A launch covers
+// tiles [a.tile0, a.tile1); block b works on the K tiles from
+// a.tile0 + b*K.
 template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
 __global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
     StepArgs a)
@@ -601,12 +668,10 @@ __global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C, FULL
         __syncthreads();
     }
     float4* xfer = smem + table_floats(G) / 4;
-    TilePos t;
-    t.tile = a.tile0 + blockIdx.x;
-    t.base = t.tile * C * kChunk;
-    const int64_t rem = (a.d - t.base + kChunk - 1) / kChunk;
-    t.nch = rem < C ? (int)rem : C;
-    round_tile<C, VEC, FULL, QW, QS, PL>(a, t, lut_w, lut_s, xfer, G);
+    constexpr int K = round_tiles_per_block(C, FULL && PL == AT_SERVER);
+    const int64_t first = a.tile0 + (int64_t)blockIdx.x * K;
+    const int64_t left = a.tile1 - first;
+    round_tiles<C, K, VEC, FULL, QW, QS, PL>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G);
 }
 
 // Per-tile partial norms of the worker inputs p for workers [i0, i1), without
@@ -693,8 +758,10 @@ __global__ __launch_bounds__(kBlock) void worker_kernel(StepArgs a)
     worker_p<C, -1>(a, r, p);
     if (atw) store_moments<C, VEC, false, -1>(a, a.m_w, a.v_w, t.base, t.nch, r);
     const float gs = wglobal ? a.wscales[0] : 0.0f;
+    WordSink sink = message_sink<QRt>(a.qw, a.wcodes, t.base);
     quantize_tile<C, false, QRt>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)a.worker, gs,
-                                 a.wcodes, a.wscales, dq);
+                                 a.wcodes, a.wscales, sink, dq);
+    sink.flush();
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         if (ch >= t.nch) continue;
@@ -750,8 +817,10 @@ __global__ __launch_bounds__(kBlock) void server_kernel(StepArgs a)
         q[ch] = add4(ld4<VEC>(a.ubuf, n, a.d), ld4<VEC>(a.e_s, n, a.d));
     }
     const float gs = sglobal ? a.sscales[0] : 0.0f;
+    WordSink sink = message_sink<QRt>(a.qs, a.scodes, t.base);
     quantize_tile<C, false, QRt>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, gs, a.scodes,
-                                 a.sscales, dq);
+                                 a.sscales, sink, dq);
+    sink.flush();
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         if (ch >= t.nch) continue;
@@ -823,13 +892,16 @@ struct Special {
     int wkind, wbits, wnorm, wcpb;
     int skind, sbits, snorm, scpb;
     int placement;
-    void (*kernel)(StepArgs);
+    void (*kernel)(StepArgs);   // whole tiles
+    void (*edge)(StepArgs);     // the ragged last tile
+    int tiles;                  // tiles per block of `kernel`
 };
 
 #define EA_SPECIAL(CC, QWT, QST, PLC)                                                               \
     Special{CC, QWT::kind(QDev{}), QWT::bits(QDev{}), QWT::norm(QDev{}), QWT::cpb(QDev{}),         \
             QST::kind(QDev{}), QST::bits(QDev{}), QST::norm(QDev{}), QST::cpb(QDev{}), PLC,         \
-            step_kernel<CC, true, true, QWT, QST, PLC>}
+            step_kernel<CC, true, true, QWT, QST, PLC>, step_kernel<CC, true, false, QWT, QST, PLC>,         \
+            round_tiles_per_block(CC, PLC == AT_SERVER)}
 
 const Special kSpecials[] = {
     EA_SPECIAL(2, Stoch4L2Q2, Stoch4L2Q2, AT_SERVER),
@@ -856,21 +928,23 @@ const Special* find_special(const StepArgs& a, int C)
 
 }  // namespace
 
-// Whole tiles go to a kernel without bounds checks (specialized when one
-// matches the configuration); the ragged last tile, and every tile of rows
-// that are not 16-byte aligned, go to the generic checked kernel.
+// Whole tiles go to a kernel without bounds checks and the ragged last tile
+// to a checked one, both specialized when one matches the configuration;
+// every tile of rows that are not 16-byte aligned goes to the generic checked
+// kernel.
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
     const size_t limit = lds_limit_bytes();
-    const int G = round_waves(a.N, C, limit);
-    const dim3 block((unsigned)(G * kWave));
-    const size_t lds = round_lds_bytes(a.N, C, G);
     const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) : 0;
+    const Special* sp = vec ? find_special(a, C) : nullptr;
     if (nfull > 0) {
+        const int K = sp ? sp->tiles : round_tiles_per_block(C, false);
+        const int G = round_waves(a.N, C, K, limit);
         StepArgs b = a;
         b.tile0 = 0;
-        const dim3 grid((unsigned)nfull);
-        const Special* sp = find_special(a, C);
+        b.tile1 = nfull;
+        const dim3 grid((unsigned)((nfull + K - 1) / K)), block((unsigned)(G * kWave));
+        const size_t lds = round_lds_bytes(a.N, C, G, K);
         if (sp) {
             hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
         } else {
@@ -886,9 +960,16 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
         if (e != hipSuccess) return e;
     }
     if (nfull < a.ntiles) {
+        const int G = round_waves(a.N, C, 1, limit);
         StepArgs b = a;
         b.tile0 = nfull;
-        const dim3 grid((unsigned)(a.ntiles - nfull));
+        b.tile1 = a.ntiles;
+        const dim3 grid((unsigned)(a.ntiles - nfull)), block((unsigned)(G * kWave));
+        const size_t lds = round_lds_bytes(a.N, C, G, 1);
+        if (sp) {
+            hipLaunchKernelGGL(sp->edge, grid, block, lds, s, b);
+            return hipGetLastError();
+        }
         switch (C) {
         case 1: hipLaunchKernelGGL((step_kernel<1, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
         case 2: hipLaunchKernelGGL((step_kernel<2, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;

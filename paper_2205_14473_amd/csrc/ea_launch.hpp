@@ -38,7 +38,7 @@ struct StepArgs {
     double* wpart;            // [N][ntiles] per-tile partial norms (qw one bucket)
     double* spart;            // [ntiles]    per-tile partial norms (qs one bucket)
     float* ubuf;              // [d] server input / aggregate output
-    int64_t tile0;            // fused round: tile of the launch's first block
+    int64_t tile0, tile1;     // fused round: the launch's tiles [tile0, tile1)
     int32_t worker;           // split calls: worker index (Philox stream)
     int32_t apply;            // server_kernel: also update x
 };
