@@ -133,3 +133,28 @@ def test_zero_gradients_give_zero_scales():
     g[:, 700:900] = 1e-3
     for t in range(1, 4):
         pair.step(t, g)
+
+
+# Lean whole-tile kernels take two consecutive tiles per block: odd and even
+# tile counts, with and without a ragged tail, a single tile, and more workers
+# than waves per block (double-buffered handoff).
+@pytest.mark.parametrize("d", [512 * 41 + 384, 512 * 41, 512 * 42, 512 + 100, 512, 1024 * 3])
+def test_two_tile_blocks(d):
+    _run(d, 16, STOCH(4, O.SCALE_L2, 512), STOCH(4, O.SCALE_L2, 512), O.ADAM_AT_SERVER, T=3)
+
+
+def test_two_tile_blocks_many_workers():
+    _run(512 * 7 + 200, 32, STOCH(2, O.SCALE_MAX, 512), STOCH(2, O.SCALE_MAX, 512), O.ADAM_AT_SERVER, T=3)
+    _run(512 * 5, 20, SIGN(512), SIGN(512), O.ADAM_AT_SERVER, T=3)
+
+
+def test_zero_buckets_in_lean_kernels():
+    """Buckets whose scale is zero take the wave-uniform branch of the
+    specialized kernels (bert quantizers, Adam at the server)."""
+    d, N = 512 * 9, 16
+    pair = Pair(d, N, STOCH(4, O.SCALE_L2, 512), STOCH(4, O.SCALE_L2, 512), O.ADAM_AT_SERVER, eps=0.0)
+    g = np.zeros((N, d), np.float32)
+    g[:, 1100:1700] = 1e-3
+    g[3, 3000:3100] = -2e-3
+    for t in range(1, 4):
+        pair.step(t, g)
