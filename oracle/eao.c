@@ -412,6 +412,42 @@ float eao_adam_update(float lr, float m, float v)
  * The N worker replicas of x are identical (same x_1, same broadcast), so one
  * x is kept.
  * ------------------------------------------------------------------------- */
+/* Schedules: Assumption 2's theta_t = 1 - theta/T and alpha_t = alpha/sqrt(T);
+ * Section V-B's decay of alpha by a constant factor every `period` steps. */
+int eao_schedule_at(const eao_schedule *s, float lr0, float beta2_0, int64_t t,
+                    float *lr, float *beta2)
+{
+    if (t < 1) return -1;
+    switch (s->kind) {
+    case EAO_SCHED_CONSTANT:
+        *lr = lr0;
+        *beta2 = beta2_0;
+        return 0;
+    case EAO_SCHED_ASSUMPTION2: {
+        if (s->T < 1 || s->T >= (1 << 24) || !(s->theta > 0.0f) || !(s->theta <= (float)s->T)) return -1;
+        const float Tf = (float)s->T;      /* exact: T < 2^24 */
+        *lr = s->alpha / sqrtf(Tf);
+        *beta2 = 1.0f - s->theta / Tf;
+        return 0;
+    }
+    case EAO_SCHED_STEP_DECAY: {
+        if (s->period < 1 || !(s->factor > 0.0f) || !(s->factor <= 1.0f)) return -1;
+        int64_t k = (t - 1) / s->period;
+        float r = 1.0f, b = s->factor;
+        while (k > 0) {
+            if (k & 1) r = r * b;
+            b = b * b;
+            k >>= 1;
+        }
+        *lr = s->alpha * r;
+        *beta2 = beta2_0;
+        return 0;
+    }
+    default:
+        return -1;
+    }
+}
+
 static int check_segment(const eao_quant *q, int64_t d, int64_t n0, int64_t len)
 {
     const int64_t B = eao_bucket_len(q, d);

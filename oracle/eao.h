@@ -100,6 +100,31 @@ void eao_adam_moments(float beta1, float beta2, float *m, float *v, float g);
 /* Adam step alpha * m / sqrt(v); 0 when v is not positive. */
 float eao_adam_update(float lr, float m, float v);
 
+/* Step-size schedules.  lr_t and beta2_t (the paper's alpha_t and theta_t)
+ * at step t >= 1, in binary32 arithmetic:
+ *   CONSTANT     lr0, beta2_0 (the constants of the Section V experiments);
+ *   ASSUMPTION2  alpha_t = alpha / sqrt(T), theta_t = 1 - theta / T for a
+ *                horizon of T steps (Assumption 2);
+ *   STEP_DECAY   alpha_t = alpha * factor^k with k = (t-1) / period (integer
+ *                division; Section V-B reduces alpha to 0.2 alpha after every
+ *                19,550 iterations), theta_t = beta2_0.  factor^k is formed by
+ *                square-and-multiply over the bits of k from the lowest:
+ *                r = 1, b = factor; for each bit: if set r = r*b; b = b*b.
+ * Pinned by closed forms of both formulas and by the decay boundaries.
+ * Returns 0, or -1 for an invalid schedule or t < 1. */
+enum { EAO_SCHED_CONSTANT = 0, EAO_SCHED_ASSUMPTION2 = 1, EAO_SCHED_STEP_DECAY = 2 };
+typedef struct {
+    int32_t kind;            /* EAO_SCHED_*                                     */
+    float alpha;             /* base learning rate                              */
+    float theta;             /* ASSUMPTION2: theta, 0 < theta <= T              */
+    float factor;            /* STEP_DECAY: 0 < factor <= 1                     */
+    int64_t T;               /* ASSUMPTION2: horizon, 1 <= T < 2^24             */
+    int64_t period;          /* STEP_DECAY: steps between decays, >= 1          */
+} eao_schedule;
+
+int eao_schedule_at(const eao_schedule *s, float lr0, float beta2_0, int64_t t,
+                    float *lr, float *beta2);
+
 /* One full round at step t (1-based) on the segment [n0, n0+len) of the
  * d-vector.  Arrays are segment-local:
  *   g, e_w            [N][len]   gradients; worker residuals (in/out)

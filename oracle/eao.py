@@ -15,6 +15,7 @@ from .build import ensure_built
 Q_NONE, Q_SCALED_SIGN, Q_STOCH_UNIFORM, Q_DET_UNIFORM, Q_POW2 = 0, 1, 2, 3, 4
 SCALE_L1, SCALE_L2, SCALE_MAX = 0, 1, 2
 ADAM_AT_SERVER, ADAM_AT_WORKER = 0, 1
+SCHED_CONSTANT, SCHED_ASSUMPTION2, SCHED_STEP_DECAY = 0, 1, 2
 
 
 class Quant(C.Structure):
@@ -29,7 +30,12 @@ class Config(C.Structure):
                 ("eps", C.c_float), ("seed", C.c_uint64), ("qw", Quant), ("qs", Quant)]
 
 
-assert C.sizeof(Quant) == 32 and C.sizeof(Config) == 104
+class Schedule(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("alpha", C.c_float), ("theta", C.c_float), ("factor", C.c_float),
+                ("T", C.c_int64), ("period", C.c_int64)]
+
+
+assert C.sizeof(Quant) == 32 and C.sizeof(Config) == 104 and C.sizeof(Schedule) == 32
 
 _lib = None
 
@@ -60,6 +66,8 @@ def lib():
         L.eao_adam_update.restype = C.c_float
         L.eao_step.argtypes = [C.POINTER(Config), C.c_uint32, C.c_int64, C.c_int64] + [P] * 13
         L.eao_step.restype = C.c_int
+        L.eao_schedule_at.argtypes = [C.POINTER(Schedule), C.c_float, C.c_float, C.c_int64, P, P]
+        L.eao_schedule_at.restype = C.c_int
         _lib = L
     return _lib
 
@@ -150,6 +158,16 @@ def adam_moments(beta1: float, beta2: float, m: float, v: float, g: float):
     vv = np.array([v], np.float32)
     lib().eao_adam_moments(beta1, beta2, _ptr(mm), _ptr(vv), g)
     return float(mm[0]), float(vv[0])
+
+
+def schedule_at(s: Schedule, lr0: float, beta2_0: float, t: int):
+    """(lr_t, beta2_t) as binary32 numpy scalars; ValueError for an invalid
+    schedule (Assumption 2; Section V-B step decay)."""
+    lr = np.zeros(1, np.float32)
+    b2 = np.zeros(1, np.float32)
+    if lib().eao_schedule_at(C.byref(s), lr0, beta2_0, t, _ptr(lr), _ptr(b2)) != 0:
+        raise ValueError("invalid schedule")
+    return lr[0], b2[0]
 
 
 def adam_update(lr: float, m: float, v: float) -> float:

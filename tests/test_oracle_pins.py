@@ -405,6 +405,80 @@ def test_lemma1_invariant():
 
 
 # ---------------------------------------------------------------------------
+# Schedules: Assumption 2 (theta_t = 1 - theta/T, alpha_t = alpha/sqrt(T)) and
+# the step decay of Section V-B, against their closed forms.
+# ---------------------------------------------------------------------------
+ULP = 2.0 ** -23
+
+
+def sched_(kind, alpha=0.0, theta=0.0, factor=1.0, T=0, period=1):
+    return O.Schedule(kind=kind, alpha=alpha, theta=theta, factor=factor, T=T, period=period)
+
+
+def test_schedule_constant_returns_the_configured_values():
+    s = sched_(O.SCHED_CONSTANT)
+    for t in (1, 2, 10 ** 6):
+        lr, b2 = O.schedule_at(s, 1e-3, 0.999, t)
+        assert lr == np.float32(1e-3) and b2 == np.float32(0.999)
+
+
+@pytest.mark.parametrize("alpha,theta,T", [(1e-3, 0.99, 1000), (0.05, 0.5, 19550), (1.0, 1.0, 1), (3e-4, 7.0, 12345)])
+def test_schedule_assumption2_closed_form(alpha, theta, T):
+    s = sched_(O.SCHED_ASSUMPTION2, alpha=alpha, theta=theta, T=T)
+    a32, th32 = float(np.float32(alpha)), float(np.float32(theta))
+    for t in (1, 2, T, T + 5):       # constant over t for a fixed horizon
+        lr, b2 = O.schedule_at(s, 0.0, 0.0, t)
+        assert abs(lr - a32 / math.sqrt(T)) <= 2 * ULP * (a32 / math.sqrt(T))
+        assert abs(b2 - (1.0 - th32 / T)) <= 2 * ULP
+        assert 0.0 <= b2 < 1.0
+
+
+def test_schedule_step_decay_section_vb():
+    cfg = GOLDEN["schedules"]
+    factor, period = cfg["step_decay_factor"], cfg["step_decay_period"]
+    alpha = 1e-3
+    s = sched_(O.SCHED_STEP_DECAY, alpha=alpha, factor=factor, period=period)
+    a32, f32 = float(np.float32(alpha)), float(np.float32(factor))
+    # the first `period` iterations use alpha; the decay applies after them
+    assert O.schedule_at(s, 0.0, 0.999, 1) == (np.float32(alpha), np.float32(0.999))
+    assert O.schedule_at(s, 0.0, 0.999, period)[0] == np.float32(alpha)
+    assert O.schedule_at(s, 0.0, 0.999, period + 1)[0] == np.float32(np.float32(alpha) * np.float32(factor))
+    prev = math.inf
+    for k in range(0, 40):
+        for t in (k * period + 1, (k + 1) * period):
+            lr, b2 = O.schedule_at(s, 0.0, 0.999, t)
+            want = a32 * f32 ** k
+            assert abs(lr - want) <= (2 * k.bit_length() + 2) * ULP * want + 1e-45
+            assert b2 == np.float32(0.999)
+            assert lr <= prev
+            prev = lr
+
+
+def test_schedule_step_decay_unit_factor_and_short_period():
+    s = sched_(O.SCHED_STEP_DECAY, alpha=0.1, factor=1.0, period=1)
+    assert all(O.schedule_at(s, 0.0, 0.9, t)[0] == np.float32(0.1) for t in (1, 2, 1000, 10 ** 9))
+    s = sched_(O.SCHED_STEP_DECAY, alpha=1.0, factor=0.5, period=1)
+    for t in (1, 2, 3, 30, 126, 127):
+        assert O.schedule_at(s, 0.0, 0.9, t)[0] == np.float32(2.0 ** -(t - 1))
+
+
+@pytest.mark.parametrize("s,t", [
+    (sched_(O.SCHED_CONSTANT), 0),
+    (sched_(O.SCHED_ASSUMPTION2, alpha=1e-3, theta=0.5, T=0), 1),
+    (sched_(O.SCHED_ASSUMPTION2, alpha=1e-3, theta=2.0, T=1), 1),
+    (sched_(O.SCHED_ASSUMPTION2, alpha=1e-3, theta=0.0, T=10), 1),
+    (sched_(O.SCHED_ASSUMPTION2, alpha=1e-3, theta=0.5, T=1 << 24), 1),
+    (sched_(O.SCHED_STEP_DECAY, alpha=1e-3, factor=1.5, period=10), 1),
+    (sched_(O.SCHED_STEP_DECAY, alpha=1e-3, factor=0.0, period=10), 1),
+    (sched_(O.SCHED_STEP_DECAY, alpha=1e-3, factor=0.2, period=0), 1),
+    (sched_(7), 1),
+])
+def test_schedule_rejects_invalid(s, t):
+    with pytest.raises(ValueError):
+        O.schedule_at(s, 1e-3, 0.999, t)
+
+
+# ---------------------------------------------------------------------------
 # Error feedback: telescoping identities of Section IV (EF as delayed update)
 # and the virtual-iterate identities of the appendix (Notation 1), with the
 # sign of the second identity read as x_{t+1} - e_{t+1} = x_t - e_t - avg_t.
