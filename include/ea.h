@@ -188,6 +188,59 @@ int ea_step(const ea_config_t *c, int64_t t, const float *g, float *e_w, float *
             float *m, float *v, float *e_s, float *x, uint64_t *wcodes, float *wscales,
             uint64_t *scodes, float *sscales, void *workspace, void *stream);
 
+/* ---- step-size schedules and multi-step calls ------------------------------ */
+
+/* lr_t and beta2_t (the paper's alpha_t and theta_t) at step t >= 1, in
+ * binary32 arithmetic:
+ *   EA_SCHED_CONSTANT     c->lr and c->beta2 (the Section V experiments);
+ *   EA_SCHED_ASSUMPTION2  alpha_t = alpha / sqrt(T), theta_t = 1 - theta / T for
+ *                         a horizon of T steps (Assumption 2); 1 <= T < 2^24,
+ *                         0 < theta <= T;
+ *   EA_SCHED_STEP_DECAY   alpha_t = alpha * factor^k, k = (t-1) / period, and
+ *                         theta_t = c->beta2 (Section V-B: alpha becomes
+ *                         0.2 alpha after every 19,550 iterations); factor^k is
+ *                         formed by square-and-multiply over the bits of k from
+ *                         the lowest; 0 < factor <= 1, period >= 1. */
+#define EA_SCHED_CONSTANT 0
+#define EA_SCHED_ASSUMPTION2 1
+#define EA_SCHED_STEP_DECAY 2
+
+typedef struct ea_schedule {
+    int32_t kind;            /* EA_SCHED_*                                            */
+    float alpha;             /* base learning rate (ASSUMPTION2, STEP_DECAY)          */
+    float theta;             /* ASSUMPTION2                                           */
+    float factor;            /* STEP_DECAY                                            */
+    int64_t T;               /* ASSUMPTION2: horizon                                  */
+    int64_t period;          /* STEP_DECAY: steps between decays                      */
+} ea_schedule_t;
+
+/* Host-only: (lr_t, beta2_t) of the schedule at step t >= 1 (host pointers). */
+int ea_schedule_at(const ea_config_t *c, const ea_schedule_t *s, int64_t t, float *lr, float *beta2);
+
+/* One round like ea_step, with the step index read on the device and the
+ * hyperparameters taken from the schedule:
+ *   t_dev (device, one uint32, read/write) holds the step t (>= 1; 0 gives an
+ *   undefined round); the round uses t for its draws and lr_t, beta2_t from
+ *   `s`, then stores t + 1.  Nothing on the host depends on t, so the call can
+ *   be captured once into a HIP graph and replayed, each replay taking the
+ *   next step.  Other arguments as ea_step (c->lr, c->beta2 are used by
+ *   EA_SCHED_CONSTANT only). */
+int ea_step_scheduled(const ea_config_t *c, const ea_schedule_t *s, uint32_t *t_dev, const float *g,
+                      float *e_w, float *m_w, float *v_w, float *m, float *v, float *e_s, float *x,
+                      uint64_t *wcodes, float *wscales, uint64_t *scodes, float *sscales,
+                      void *workspace, void *stream);
+
+/* `steps` rounds at t0, t0+1, ... with lr_t, beta2_t from the schedule,
+ * enqueued back to back with the state kept in device memory.  Round t0+k
+ * reads its gradients at g + k*g_step_stride (elements; 0: the same [N][d]
+ * gradients every round).  The messages of the last round are left in
+ * wcodes, wscales, scodes, sscales.  Other arguments as ea_step;
+ * 1 <= t0 and t0 + steps - 1 <= 2^32-1. */
+int ea_run(const ea_config_t *c, const ea_schedule_t *s, int64_t t0, int64_t steps, const float *g,
+           int64_t g_step_stride, float *e_w, float *m_w, float *v_w, float *m, float *v, float *e_s,
+           float *x, uint64_t *wcodes, float *wscales, uint64_t *scodes, float *sscales, void *workspace,
+           void *stream);
+
 #ifdef __cplusplus
 }
 #endif

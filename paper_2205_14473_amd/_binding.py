@@ -16,6 +16,7 @@ EA_OK, EA_ERR_ARG, EA_ERR_ALIGN, EA_ERR_HIP, EA_ERR_UNSUPPORTED = 0, -1, -2, -3,
 EA_Q_NONE, EA_Q_SCALED_SIGN, EA_Q_STOCH_UNIFORM, EA_Q_DET_UNIFORM, EA_Q_POW2 = 0, 1, 2, 3, 4
 EA_SCALE_L1, EA_SCALE_L2, EA_SCALE_MAX = 0, 1, 2
 EA_ADAM_AT_SERVER, EA_ADAM_AT_WORKER = 0, 1
+EA_SCHED_CONSTANT, EA_SCHED_ASSUMPTION2, EA_SCHED_STEP_DECAY = 0, 1, 2
 
 
 class Quant(C.Structure):
@@ -32,6 +33,15 @@ class Config(C.Structure):
                 ("seed", C.c_uint64), ("qw", Quant), ("qs", Quant)]
 
 
+class Schedule(C.Structure):
+    """ea_schedule_t"""
+    _fields_ = [("kind", C.c_int32), ("alpha", C.c_float), ("theta", C.c_float), ("factor", C.c_float),
+                ("T", C.c_int64), ("period", C.c_int64)]
+
+
+assert C.sizeof(Quant) == 32 and C.sizeof(Config) == 104 and C.sizeof(Schedule) == 32
+
+
 class EAError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"libea error {code}: {msg}")
@@ -44,7 +54,7 @@ def _load():
                           "(hipcc --offload-arch=gfx950) first")
     L = C.CDLL(LIB_PATH)
     P, I32, I64 = C.c_void_p, C.c_int32, C.c_int64
-    QP, CP = C.POINTER(Quant), C.POINTER(Config)
+    QP, CP, SP = C.POINTER(Quant), C.POINTER(Config), C.POINTER(Schedule)
     sig = {
         "ea_code_bits": (I32, [QP]),
         "ea_msg_words": (I64, [QP, I64]),
@@ -59,6 +69,9 @@ def _load():
         "ea_server_compress": (C.c_int, [CP, I64, P, P, P, P, P, P]),
         "ea_worker_apply": (C.c_int, [CP, P, P, P, P]),
         "ea_step": (C.c_int, [CP, I64] + [P] * 14),
+        "ea_schedule_at": (C.c_int, [CP, SP, I64, P, P]),
+        "ea_step_scheduled": (C.c_int, [CP, SP] + [P] * 15),
+        "ea_run": (C.c_int, [CP, SP, I64, I64, P, I64] + [P] * 13),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -174,3 +187,36 @@ def ea_step(cfg, t, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes, ssc
                               _ptr(m, f), _ptr(v, f), _ptr(e_s, f), _ptr(x, f), _ptr(wcodes, u),
                               _ptr(wscales, f), _ptr(scodes, u), _ptr(sscales, f), _ptr(workspace),
                               _stream(stream)))
+
+
+def ea_schedule_at(cfg, sched, t):
+    """(lr_t, beta2_t) of the schedule at step t, as Python floats of binary32 values."""
+    lr, b2 = C.c_float(), C.c_float()
+    _check(lib.ea_schedule_at(C.byref(cfg), C.byref(sched), t, C.byref(lr), C.byref(b2)))
+    return lr.value, b2.value
+
+
+def _ptr_u32(t):
+    if t is None or isinstance(t, int):
+        return t
+    if t.element_size() != 4 or t.is_floating_point():
+        raise ValueError("t_dev must be a 4-byte integer tensor")
+    return _ptr(t)
+
+
+def ea_step_scheduled(cfg, sched, t_dev, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes, sscales,
+                      workspace=None, stream=None):
+    f, u = _f32(), _u64()
+    return _check(lib.ea_step_scheduled(C.byref(cfg), C.byref(sched), _ptr_u32(t_dev), _ptr(g, f), _ptr(e_w, f),
+                                        _ptr(m_w, f), _ptr(v_w, f), _ptr(m, f), _ptr(v, f), _ptr(e_s, f),
+                                        _ptr(x, f), _ptr(wcodes, u), _ptr(wscales, f), _ptr(scodes, u),
+                                        _ptr(sscales, f), _ptr(workspace), _stream(stream)))
+
+
+def ea_run(cfg, sched, t0, steps, g, g_step_stride, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes,
+           sscales, workspace=None, stream=None):
+    f, u = _f32(), _u64()
+    return _check(lib.ea_run(C.byref(cfg), C.byref(sched), t0, steps, _ptr(g, f), g_step_stride, _ptr(e_w, f),
+                             _ptr(m_w, f), _ptr(v_w, f), _ptr(m, f), _ptr(v, f), _ptr(e_s, f), _ptr(x, f),
+                             _ptr(wcodes, u), _ptr(wscales, f), _ptr(scodes, u), _ptr(sscales, f),
+                             _ptr(workspace), _stream(stream)))

@@ -204,6 +204,52 @@ int check_t(int64_t t)
     return EA_OK;
 }
 
+// Schedules (declared with their definition in ea.h).
+int check_schedule(const ea_schedule_t* s)
+{
+    if (!s) return fail(EA_ERR_ARG, "schedule is NULL");
+    switch (s->kind) {
+    case EA_SCHED_CONSTANT:
+        return EA_OK;
+    case EA_SCHED_ASSUMPTION2:
+        if (s->T < 1 || s->T >= ((int64_t)1 << 24))
+            return fail(EA_ERR_ARG, "schedule horizon T must be in [1, 2^24) (got %lld)", (long long)s->T);
+        if (!(s->theta > 0.0f) || !(s->theta <= (float)s->T))
+            return fail(EA_ERR_ARG, "schedule theta must be in (0, T] (got %g)", (double)s->theta);
+        break;
+    case EA_SCHED_STEP_DECAY:
+        if (s->period < 1) return fail(EA_ERR_ARG, "schedule period must be >= 1 (got %lld)", (long long)s->period);
+        if (!(s->factor > 0.0f) || !(s->factor <= 1.0f))
+            return fail(EA_ERR_ARG, "schedule factor must be in (0, 1] (got %g)", (double)s->factor);
+        break;
+    default:
+        return fail(EA_ERR_ARG, "unknown schedule kind %d", s->kind);
+    }
+    if (!std::isfinite(s->alpha) || s->alpha < 0.0f)
+        return fail(EA_ERR_ARG, "schedule alpha must be finite and >= 0 (got %g)", (double)s->alpha);
+    return EA_OK;
+}
+
+// lr_t, beta2_t of a validated schedule at step t >= 1, in binary32.
+void schedule_values(const ea_schedule_t* s, float lr0, float beta2_0, int64_t t, float* lr, float* beta2)
+{
+    *lr = lr0;
+    *beta2 = beta2_0;
+    if (s->kind == EA_SCHED_ASSUMPTION2) {
+        const float Tf = (float)s->T;
+        *lr = s->alpha / std::sqrt(Tf);
+        *beta2 = 1.0f - s->theta / Tf;
+    } else if (s->kind == EA_SCHED_STEP_DECAY) {
+        int64_t k = (t - 1) / s->period;
+        float r = 1.0f, b = s->factor;
+        for (; k > 0; k >>= 1) {
+            if (k & 1) r = r * b;
+            b = b * b;
+        }
+        *lr = s->alpha * r;
+    }
+}
+
 int hip_status(hipError_t e, const char* what)
 {
     if (e != hipSuccess) return fail(EA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -230,6 +276,77 @@ bool vec_ok(int64_t d, std::initializer_list<const void*> ptrs)
     for (const void* q : ptrs)
         if (q && !aligned(q, 16)) return false;
     return true;
+}
+
+// One fused round.  With t_dev the step is read on the device, lr and beta2
+// come from the schedule at that step, and t_dev is advanced afterwards.
+int step_impl(const char* name, const ea_config_t* c, int64_t t, uint32_t* t_dev, const ea_schedule_t* sched,
+              const float* g, float* e_w, float* m_w, float* v_w, float* m, float* v, float* e_s, float* x,
+              uint64_t* wcodes, float* wscales, uint64_t* scodes, float* sscales, void* workspace, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    if (!t_dev && (rc = check_t(t))) return rc;
+    const bool srv = c->placement == EA_ADAM_AT_SERVER;
+    PtrCheck pc;
+    pc.need(g, true, 4, "g");
+    pc.need(e_w, true, 4, "e_w");
+    pc.need(m_w, !srv, 4, "m_w");
+    pc.need(v_w, !srv, 4, "v_w");
+    pc.need(m, srv, 4, "m");
+    pc.need(v, srv, 4, "v");
+    pc.need(e_s, true, 4, "e_s");
+    pc.need(x, true, 4, "x");
+    pc.need(wcodes, true, 8, "wcodes");
+    pc.need(wscales, p.qw.nscales > 0, 4, "wscales");
+    pc.need(scodes, true, 8, "scodes");
+    pc.need(sscales, p.qs.nscales > 0, 4, "sscales");
+    pc.need(workspace, p.ws_bytes > 0, 256, "workspace");
+    if (pc.rc) return pc.rc;
+    ea::StepArgs a = base_args(c, p, t);
+    if (t_dev) {
+        a.t_dev = t_dev;
+        a.sched_kind = sched->kind;
+        a.sched_alpha = sched->alpha;
+        a.sched_theta = sched->theta;
+        a.sched_factor = sched->factor;
+        a.sched_T = sched->T;
+        a.sched_period = sched->period;
+    }
+    a.g = g;
+    a.e_w = e_w;
+    a.m_w = srv ? nullptr : m_w;
+    a.v_w = srv ? nullptr : v_w;
+    a.m = srv ? m : nullptr;
+    a.v = srv ? v : nullptr;
+    a.e_s = e_s;
+    a.x = x;
+    a.wcodes = wcodes;
+    a.wscales = wscales;
+    a.scodes = scodes;
+    a.sscales = sscales;
+    a.apply = 1;
+    if (p.wglobal) a.wpart = (double*)((char*)workspace + p.off_wpart);
+    if (p.sglobal) {
+        a.spart = (double*)((char*)workspace + p.off_spart);
+        a.ubuf = (float*)((char*)workspace + p.off_ubuf);
+    }
+    const bool vec = vec_ok(c->d, {g, e_w, a.m_w, a.v_w, a.m, a.v, e_s, x, a.ubuf});
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipSuccess;
+    if (p.wglobal) {
+        e = ea::launch_worker_partials(a, p.C, vec, 0, c->N, s);
+        if (e == hipSuccess)
+            e = ea::launch_finalize(a.wpart, p.ntiles, p.qw.norm, c->d, wscales, p.qw.nscales, c->N, s);
+    }
+    if (e == hipSuccess) e = ea::launch_step(a, p.C, vec, s);
+    if (e == hipSuccess && p.sglobal) {
+        e = ea::launch_finalize(a.spart, p.ntiles, p.qs.norm, c->d, sscales, 1, 1, s);
+        if (e == hipSuccess) e = ea::launch_server(a, p.C, vec, s);
+    }
+    if (e == hipSuccess && t_dev) e = ea::launch_advance(t_dev, s);
+    return hip_status(e, name);
 }
 
 }  // namespace
@@ -426,59 +543,59 @@ int ea_step(const ea_config_t* c, int64_t t, const float* g, float* e_w, float* 
             float* v, float* e_s, float* x, uint64_t* wcodes, float* wscales, uint64_t* scodes, float* sscales,
             void* workspace, void* stream)
 {
-    Plan p;
-    int rc = make_plan(c, &p);
+    return step_impl("ea_step", c, t, nullptr, nullptr, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes,
+                     sscales, workspace, stream);
+}
+
+int ea_schedule_at(const ea_config_t* c, const ea_schedule_t* s, int64_t t, float* lr, float* beta2)
+{
+    if (!c || !lr || !beta2) return fail(EA_ERR_ARG, "ea_schedule_at: NULL argument");
+    int rc = check_schedule(s);
     if (rc) return rc;
-    if ((rc = check_t(t))) return rc;
-    const bool srv = c->placement == EA_ADAM_AT_SERVER;
-    PtrCheck pc;
-    pc.need(g, true, 4, "g");
-    pc.need(e_w, true, 4, "e_w");
-    pc.need(m_w, !srv, 4, "m_w");
-    pc.need(v_w, !srv, 4, "v_w");
-    pc.need(m, srv, 4, "m");
-    pc.need(v, srv, 4, "v");
-    pc.need(e_s, true, 4, "e_s");
-    pc.need(x, true, 4, "x");
-    pc.need(wcodes, true, 8, "wcodes");
-    pc.need(wscales, p.qw.nscales > 0, 4, "wscales");
-    pc.need(scodes, true, 8, "scodes");
-    pc.need(sscales, p.qs.nscales > 0, 4, "sscales");
-    pc.need(workspace, p.ws_bytes > 0, 256, "workspace");
-    if (pc.rc) return pc.rc;
-    ea::StepArgs a = base_args(c, p, t);
-    a.g = g;
-    a.e_w = e_w;
-    a.m_w = srv ? nullptr : m_w;
-    a.v_w = srv ? nullptr : v_w;
-    a.m = srv ? m : nullptr;
-    a.v = srv ? v : nullptr;
-    a.e_s = e_s;
-    a.x = x;
-    a.wcodes = wcodes;
-    a.wscales = wscales;
-    a.scodes = scodes;
-    a.sscales = sscales;
-    a.apply = 1;
-    if (p.wglobal) a.wpart = (double*)((char*)workspace + p.off_wpart);
-    if (p.sglobal) {
-        a.spart = (double*)((char*)workspace + p.off_spart);
-        a.ubuf = (float*)((char*)workspace + p.off_ubuf);
+    if (t < 1) return fail(EA_ERR_ARG, "t must be >= 1 (got %lld)", (long long)t);
+    schedule_values(s, c->lr, c->beta2, t, lr, beta2);
+    return ok();
+}
+
+int ea_step_scheduled(const ea_config_t* c, const ea_schedule_t* s, uint32_t* t_dev, const float* g, float* e_w,
+                      float* m_w, float* v_w, float* m, float* v, float* e_s, float* x, uint64_t* wcodes,
+                      float* wscales, uint64_t* scodes, float* sscales, void* workspace, void* stream)
+{
+    int rc = check_schedule(s);
+    if (rc) return rc;
+    if (!t_dev || ((uintptr_t)t_dev & 3u)) return fail(EA_ERR_ALIGN, "t_dev must be a 4-byte aligned device pointer");
+    return step_impl("ea_step_scheduled", c, 1, t_dev, s, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes,
+                     sscales, workspace, stream);
+}
+
+int ea_run(const ea_config_t* c, const ea_schedule_t* s, int64_t t0, int64_t steps, const float* g,
+           int64_t g_step_stride, float* e_w, float* m_w, float* v_w, float* m, float* v, float* e_s, float* x,
+           uint64_t* wcodes, float* wscales, uint64_t* scodes, float* sscales, void* workspace, void* stream)
+{
+    if (!c) return fail(EA_ERR_ARG, "config is NULL");
+    int rc = check_schedule(s);
+    if (rc) return rc;
+    if (steps < 0) return fail(EA_ERR_ARG, "steps must be >= 0 (got %lld)", (long long)steps);
+    if (g_step_stride < 0) return fail(EA_ERR_ARG, "g_step_stride must be >= 0");
+    if ((rc = check_t(t0))) return rc;
+    if (steps > 0 && (rc = check_t(t0 + steps - 1))) return rc;
+    // Validate every step's configuration before enqueueing any of them.
+    for (int64_t k = 0; k < steps; ++k) {
+        ea_config_t ck = *c;
+        schedule_values(s, c->lr, c->beta2, t0 + k, &ck.lr, &ck.beta2);
+        Plan p;
+        if ((rc = make_plan(&ck, &p))) return rc;
+        if (s->kind == EA_SCHED_CONSTANT) break;
+        if (s->kind == EA_SCHED_ASSUMPTION2) break;   // the same values at every step
     }
-    const bool vec = vec_ok(c->d, {g, e_w, a.m_w, a.v_w, a.m, a.v, e_s, x, a.ubuf});
-    hipStream_t s = (hipStream_t)stream;
-    hipError_t e = hipSuccess;
-    if (p.wglobal) {
-        e = ea::launch_worker_partials(a, p.C, vec, 0, c->N, s);
-        if (e == hipSuccess)
-            e = ea::launch_finalize(a.wpart, p.ntiles, p.qw.norm, c->d, wscales, p.qw.nscales, c->N, s);
+    for (int64_t k = 0; k < steps; ++k) {
+        ea_config_t ck = *c;
+        schedule_values(s, c->lr, c->beta2, t0 + k, &ck.lr, &ck.beta2);
+        rc = step_impl("ea_run", &ck, t0 + k, nullptr, nullptr, g ? g + k * g_step_stride : nullptr, e_w, m_w, v_w,
+                       m, v, e_s, x, wcodes, wscales, scodes, sscales, workspace, stream);
+        if (rc) return rc;
     }
-    if (e == hipSuccess) e = ea::launch_step(a, p.C, vec, s);
-    if (e == hipSuccess && p.sglobal) {
-        e = ea::launch_finalize(a.spart, p.ntiles, p.qs.norm, c->d, sscales, 1, 1, s);
-        if (e == hipSuccess) e = ea::launch_server(a, p.C, vec, s);
-    }
-    return hip_status(e, "ea_step");
+    return ok();
 }
 
 }  // extern "C"

@@ -77,6 +77,33 @@ __device__ __forceinline__ int placement_of(const StepArgs& a)
     return PL < 0 ? a.placement : PL;
 }
 
+// The launch's arguments with the step taken from the device when the round
+// reads it there (a.t_dev), and lr, beta2 from the schedule at that step
+// (Assumption 2: alpha/sqrt(T), 1 - theta/T; step decay: alpha * factor^k,
+// k = (t-1)/period, factor^k by square-and-multiply from the lowest bit).
+__device__ __forceinline__ StepArgs with_step(const StepArgs& in)
+{
+    StepArgs a = in;
+    if (a.t_dev == nullptr) return a;
+    const uint32_t t = *a.t_dev;
+    a.t = t;
+    if (a.sched_kind == EA_SCHED_ASSUMPTION2) {
+        const float Tf = (float)a.sched_T;
+        a.lr = a.sched_alpha / sqrtf(Tf);
+        a.beta2 = 1.0f - a.sched_theta / Tf;
+    } else if (a.sched_kind == EA_SCHED_STEP_DECAY) {
+        int64_t k = ((int64_t)t - 1) / a.sched_period;
+        float r = 1.0f, b = a.sched_factor;
+        while (k > 0) {
+            if (k & 1) r = r * b;
+            b = b * b;
+            k >>= 1;
+        }
+        a.lr = a.sched_alpha * r;
+    }
+    return a;
+}
+
 // ---------------------------------------------------------------------------
 // Quantize one tile: scales (reduced per bucket inside the wave, or given for
 // a one-bucket quantizer), codes, bit-plane packing and the dequantized
@@ -647,8 +674,9 @@ size_t lds_limit_bytes()
 // a.tile0 + b*K.
 template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
 __global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
-    StepArgs a)
+    StepArgs args)
 {
+    const StepArgs a = with_step(args);
     static_assert(!FULL || VEC, "whole-tile kernels need aligned rows");
     extern __shared__ float4 smem[];
     const int G = (int)(blockDim.x / kWave);
@@ -677,8 +705,9 @@ __global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C, FULL
 // Per-tile partial norms of the worker inputs p for workers [i0, i1), without
 // writing any state (one-bucket Q_w).  Rows are [i - i0][d] from a.g etc.
 template <int C, bool VEC>
-__global__ __launch_bounds__(kBlock) void worker_partials_kernel(StepArgs a, int i0, int i1)
+__global__ __launch_bounds__(kBlock) void worker_partials_kernel(StepArgs args, int i0, int i1)
 {
+    const StepArgs a = with_step(args);
     TilePos t;
     if (!tile_pos<C>(a, t)) return;
     const bool atw = a.placement == AT_WORKER;
@@ -799,8 +828,9 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
 
 // Server compression from u (a.ubuf) and e_s; optionally also x -= message.
 template <int C, bool VEC>
-__global__ __launch_bounds__(kBlock) void server_kernel(StepArgs a)
+__global__ __launch_bounds__(kBlock) void server_kernel(StepArgs args)
 {
+    const StepArgs a = with_step(args);
     __shared__ float lut_s[kLutSize];
     fill_lut(a.qs, lut_s);
     __syncthreads();
@@ -854,6 +884,11 @@ __global__ void fill_kernel(float* __restrict__ p, int64_t n, float value)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         p[i] = value;
+}
+
+__global__ void advance_kernel(uint32_t* t_dev)
+{
+    if (threadIdx.x == 0) t_dev[0] = t_dev[0] + 1u;
 }
 
 int64_t grid_of(const StepArgs& a)
@@ -1027,6 +1062,12 @@ hipError_t launch_server(const StepArgs& a, int C, bool vec, hipStream_t s)
 hipError_t launch_apply(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
     EA_DISPATCH(apply_kernel, C, vec, grid_of(a), s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_advance(uint32_t* t_dev, hipStream_t s)
+{
+    hipLaunchKernelGGL(advance_kernel, dim3(1), dim3(kWave), 0, s, t_dev);
     return hipGetLastError();
 }
 

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "ea.h"
 #include "ea_device.hpp"
 
 namespace ea {
@@ -41,6 +42,12 @@ struct StepArgs {
     int64_t tile0, tile1;     // fused round: the launch's tiles [tile0, tile1)
     int32_t worker;           // split calls: worker index (Philox stream)
     int32_t apply;            // server_kernel: also update x
+    // Step index read on the device (null: `t`, `lr`, `beta2` above hold the
+    // step's values); the schedule then gives lr and beta2 at that step.
+    const uint32_t* t_dev;
+    int32_t sched_kind;       // EA_SCHED_*
+    float sched_alpha, sched_theta, sched_factor;
+    int64_t sched_T, sched_period;
 };
 
 // Launchers; C = chunks per tile (1..8), vec = rows are 16-byte aligned.
@@ -56,5 +63,7 @@ hipError_t launch_aggregate(const StepArgs& a, int C, bool vec, hipStream_t s);
 hipError_t launch_server(const StepArgs& a, int C, bool vec, hipStream_t s);
 hipError_t launch_apply(const StepArgs& a, int C, bool vec, hipStream_t s);
 hipError_t launch_fill(float* p, int64_t n, float value, hipStream_t s);
+// t_dev[0] <- t_dev[0] + 1 (after the kernels of a round that read it).
+hipError_t launch_advance(uint32_t* t_dev, hipStream_t s);
 
 }  // namespace ea

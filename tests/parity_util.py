@@ -96,24 +96,61 @@ def _codes_match(q_o, bits, d, n0, got_words, want_words, got_scales, want_scale
 class Pair:
     """The oracle and the HIP path stepping the same configuration."""
 
-    def __init__(self, d, N, qw, qs, placement=O.ADAM_AT_SERVER, seed=1, x1=None, split=False, **hp):
+    def __init__(self, d, N, qw, qs, placement=O.ADAM_AT_SERVER, seed=1, x1=None, split=False, sched=None,
+                 mode=None, **hp):
+        """mode: "step" (ea_step), "split" (the four calls), "scheduled"
+        (ea_step_scheduled, step index on the device), "run" (ea_run, one
+        step per call) or "graph" (ea_step_scheduled captured once in a HIP
+        graph and replayed); the last three take lr, beta2 from `sched`."""
         self.oc, self.ec = configs(d, N, qw, qs, placement, seed, **hp)
+        self.mode = mode or ("split" if split else "step")
+        self.sched = sched
+        if sched is not None:
+            self.so, self.se = O.Schedule(**sched), E.Schedule(**sched)
+            self.t_dev = torch.zeros(1, dtype=torch.int32, device="cuda")
+        self.graph = None
         self.d, self.N = d, N
         x1 = np.zeros(d, np.float32) if x1 is None else np.asarray(x1, np.float32)
         self.ost = O.State.init(self.oc, d, x1)
         self.rb = allocate(self.ec, with_u=True)
         init_state(self.ec, self.rb)
         self.rb.x.copy_(torch.from_numpy(x1))
-        self.split = split
+        self.split = self.mode == "split"
         self.stats = Stats()
         self.bw, self.bs = O.code_bits(self.oc.qw), O.code_bits(self.oc.qs)
         self.nsw, self.nss = E.ea_msg_scales(self.ec.qw, d), E.ea_msg_scales(self.ec.qs, d)
         torch.cuda.synchronize()
 
+    def oracle_config(self, t):
+        if self.sched is None:
+            return self.oc
+        c = O.Config.from_buffer_copy(self.oc)
+        c.lr, c.beta2 = (float(v) for v in O.schedule_at(self.so, self.oc.lr, self.oc.beta2, t))
+        return c
+
     def gpu_step(self, t):
         rb, c = self.rb, self.ec
-        if not self.split:
+        if self.mode == "step":
             E.ea_step(c, t, **rb.step_args())
+            return
+        args = rb.step_args()
+        if self.mode == "scheduled":
+            self.t_dev.fill_(t)
+            E.ea_step_scheduled(c, self.se, self.t_dev, **args)
+            return
+        if self.mode == "run":
+            g = args.pop("g")
+            E.ea_run(c, self.se, t, 1, g, 0, **args)
+            return
+        if self.mode == "graph":
+            if self.graph is None:
+                self.t_dev.fill_(t)
+                torch.cuda.synchronize()
+                self.graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(self.graph):
+                    E.ea_step_scheduled(c, self.se, self.t_dev, **args)
+            assert int(self.t_dev.item()) == t, "graph replay out of step with the oracle"
+            self.graph.replay()
             return
         for i in range(self.N):
             E.ea_worker_compress(c, i, t, rb.g[i], rb.e_w[i], None if rb.m_w is None else rb.m_w[i],
@@ -125,10 +162,12 @@ class Pair:
 
     def step(self, t, g):
         g = np.ascontiguousarray(g, np.float32)
-        out = O.step(self.oc, t, g, self.ost, want_srv_in=self.split)
+        out = O.step(self.oracle_config(t), t, g, self.ost, want_srv_in=self.split)
         self.rb.g.copy_(torch.from_numpy(g))
         self.gpu_step(t)
         torch.cuda.synchronize()
+        if self.mode in ("scheduled", "graph"):
+            assert int(self.t_dev.item()) == t + 1, "the round did not advance its step counter"
         self.compare(out)
         self.stats.steps += 1
         return out

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(E):
     names = _declared()
-    assert len(names) == 13, names
+    assert len(names) == 16, names
     for n in names:
         assert hasattr(E.lib, n), f"{n} declared in include/ea.h but not exported"
 
@@ -120,3 +120,68 @@ def test_calls_rejected_before_device_work(E):
     c1 = _cfg(E, d=1024, N=2, qw=one, qs=one)
     assert E.lib.ea_step(ctypes.byref(c1), 1, *good[:12], None, None) == E.EA_ERR_ARG
     assert "workspace" in E.ea_last_error()
+
+
+SCHEDULES = [
+    dict(kind=0),
+    dict(kind=1, alpha=1e-3, theta=0.99, T=1000),
+    dict(kind=1, alpha=0.05, theta=3.0, T=19550),
+    dict(kind=2, alpha=1e-3, factor=0.2, period=19550),
+    dict(kind=2, alpha=0.1, factor=0.5, period=3),
+    dict(kind=2, alpha=1.0, factor=0.999, period=1),
+]
+
+
+@pytest.mark.parametrize("sd", SCHEDULES)
+def test_schedule_values_agree_with_oracle(E, sd):
+    """The library's host schedule and the oracle's are separate
+    implementations of one definition: they agree to the bit."""
+    c = _cfg(E)
+    se, so = E.Schedule(**sd), O.Schedule(**sd)
+    for t in [1, 2, 3, 4, 5, 17, 1000, 19550, 19551, 39101, 10 ** 6, 2 ** 32 - 1]:
+        lr, b2 = E.ea_schedule_at(c, se, t)
+        lo, bo = O.schedule_at(so, c.lr, c.beta2, t)
+        assert lr == float(lo) and b2 == float(bo), (t, lr, lo, b2, bo)
+
+
+@pytest.mark.parametrize("sd", [
+    dict(kind=1, alpha=1e-3, theta=0.5, T=0),
+    dict(kind=1, alpha=1e-3, theta=2.0, T=1),
+    dict(kind=1, alpha=1e-3, theta=0.0, T=10),
+    dict(kind=1, alpha=1e-3, theta=0.5, T=1 << 24),
+    dict(kind=2, alpha=1e-3, factor=1.5, period=10),
+    dict(kind=2, alpha=1e-3, factor=0.0, period=10),
+    dict(kind=2, alpha=1e-3, factor=0.2, period=0),
+    dict(kind=2, alpha=-1.0, factor=0.2, period=10),
+    dict(kind=2, alpha=float("inf"), factor=0.2, period=10),
+    dict(kind=7),
+])
+def test_invalid_schedule_rejected(E, sd):
+    with pytest.raises(E.EAError):
+        E.ea_schedule_at(_cfg(E), E.Schedule(**sd), 1)
+
+
+def test_scheduled_calls_rejected_before_device_work(E):
+    torch = pytest.importorskip("torch")
+    if torch.cuda.device_count() > 0:
+        pytest.skip("bogus-pointer rejection test runs on GPU-less hosts only")
+    c = _cfg(E, d=1024, N=2)
+    P = ctypes.c_void_p
+    good = [P(4096 * (k + 1)) for k in range(14)]
+    s = E.Schedule(kind=2, alpha=1e-3, factor=0.2, period=10)
+    bad = E.Schedule(kind=2, alpha=1e-3, factor=0.0, period=10)
+    sb = ctypes.byref
+    # the step counter must be a 4-byte aligned device pointer
+    assert E.lib.ea_step_scheduled(sb(c), sb(s), None, *good) == E.EA_ERR_ALIGN
+    assert E.lib.ea_step_scheduled(sb(c), sb(s), P(4098), *good) == E.EA_ERR_ALIGN
+    assert E.lib.ea_step_scheduled(sb(c), sb(bad), P(4096), *good) == E.EA_ERR_ARG
+    assert E.lib.ea_step_scheduled(sb(c), sb(s), P(4096), None, *good[1:]) == E.EA_ERR_ARG
+    # multi-step run: steps, first step, stride and schedule are checked up front
+    g0, rest = good[0], good[1:]
+    assert E.lib.ea_run(sb(c), sb(s), 1, -1, g0, 0, *rest) == E.EA_ERR_ARG
+    assert E.lib.ea_run(sb(c), sb(s), 0, 3, g0, 0, *rest) == E.EA_ERR_ARG
+    assert E.lib.ea_run(sb(c), sb(s), 2 ** 32 - 2, 3, g0, 0, *rest) == E.EA_ERR_ARG
+    assert E.lib.ea_run(sb(c), sb(s), 1, 3, g0, -5, *rest) == E.EA_ERR_ARG
+    assert E.lib.ea_run(sb(c), sb(bad), 1, 3, g0, 0, *rest) == E.EA_ERR_ARG
+    assert E.lib.ea_run(sb(c), sb(s), 1, 3, None, 0, *rest) == E.EA_ERR_ARG
+    assert E.lib.ea_run(sb(c), sb(s), 1, 0, g0, 0, *rest) == E.EA_OK   # nothing to do
