@@ -123,7 +123,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="bert", choices=[k for k in W.WORKLOADS if k != "toy"])
+    ap.add_argument("--workload", default="bert", choices=list(W.WORKLOADS))
+    ap.add_argument("--call", default="step", choices=["step", "scheduled", "graph"],
+                    help="time ea_step (default), ea_step_scheduled with the step on the device and a "
+                         "Section V-B step-decay schedule, or that call captured once in a HIP graph and "
+                         "replayed")
     ap.add_argument("--placement", default="server", choices=["server", "worker"])
     ap.add_argument("--cpu-sample", type=int, default=1 << 24, help="parameters in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -168,16 +172,35 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
+    sched = E.Schedule(kind=E.EA_SCHED_STEP_DECAY, alpha=cfg.lr, factor=0.2, period=19550)
+    t_dev = torch.ones(1, dtype=torch.int32, device="cuda")
+    graph = None
+    if args.call == "graph":
+        E.ea_step_scheduled(cfg, sched, t_dev, **rb.step_args(), stream=stream)   # per-device setup, step 1
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            E.ea_step_scheduled(cfg, sched, t_dev, **rb.step_args())
+        stream = torch.cuda.current_stream()
     t = 1
-    for _ in range(args.warmup):
-        E.ea_step(cfg, t, **rb.step_args(), stream=stream)
+
+    def one_round():
+        nonlocal t
+        if args.call == "step":
+            E.ea_step(cfg, t, **rb.step_args(), stream=stream)
+        elif args.call == "scheduled":
+            E.ea_step_scheduled(cfg, sched, t_dev, **rb.step_args(), stream=stream)
+        else:
+            graph.replay()
         t += 1
+
+    for _ in range(args.warmup):
+        one_round()
     torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record(stream)
     for _ in range(args.steps):
-        E.ea_step(cfg, t, **rb.step_args(), stream=stream)
-        t += 1
+        one_round()
     stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
@@ -193,7 +216,7 @@ def main():
         "metric": METRIC, "value": round(value, 4), "unit": "Gparam/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.name, "d": cfg.d, "N": cfg.N,
+        "config": {"workload": w.name, "d": cfg.d, "N": cfg.N, "call": args.call,
                    "placement": "adam_at_server" if placement == 0 else "adam_at_worker",
                    "qw": w.qw.fields(), "qs": w.qs.fields()},
         "param_workers_per_s": round(cfg.N * value, 3),

@@ -128,11 +128,13 @@ def initial_x(w: Workload, d: int = None) -> np.ndarray:
     return (np.float32(0.02) * np.random.default_rng([w.seed, 0x1]).standard_normal(d, dtype=np.float32))
 
 
-def device_gradients(w: Workload, t: int, out, d: int = None):
+def device_gradients(w: Workload, t: int, out, d: int = None, x=None, x_star=None):
     """Fill a torch tensor out[N, d] on its device with step-t gradients (torch RNG).
 
     Used where host generation of N*d values would dominate (the benchmark and
-    full-size checks); the recipe is the one in the module docstring.
+    full-size checks); the recipe is the one in the module docstring.  The toy
+    quadratic's gradient (x - x_star) + 0.1 z needs x and x_star (device
+    tensors); without them only the noise term is drawn.
     """
     import torch
     d = w.d if d is None else d
@@ -155,6 +157,10 @@ def device_gradients(w: Workload, t: int, out, d: int = None):
             hit = torch.rand(d, generator=gen, device=out.device) < 0.01
             row.mul_(1e-3)
             row[hit] *= 100.0
+        elif w.gen == "toy":
+            row.mul_(0.1)
+            if x is not None:
+                row.add_(x - x_star)
         else:
             raise ValueError(f"device generation not defined for {w.gen}")
     return out
