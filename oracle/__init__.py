@@ -8,7 +8,7 @@ paper (Section IV, Algorithms 1-2; Section III, Examples 1-2).
 from .eao import (  # noqa: F401
     Q_NONE, Q_SCALED_SIGN, Q_STOCH_UNIFORM, Q_DET_UNIFORM, Q_POW2,
     SCALE_L1, SCALE_L2, SCALE_MAX, ADAM_AT_SERVER, ADAM_AT_WORKER,
-    SCHED_CONSTANT, SCHED_ASSUMPTION2, SCHED_STEP_DECAY, Schedule, schedule_at,
+    SCHED_CONSTANT, SCHED_ASSUMPTION2, SCHED_STEP_DECAY, Schedule, schedule_at, toy_grad,
     Quant, Config, lib, philox, uniforms, code_bits, bucket_len, num_scales,
     msg_words, quantize, dequantize, pack, unpack, adam_moments, adam_update,
     State, step,

@@ -412,6 +412,41 @@ float eao_adam_update(float lr, float m, float v)
  * The N worker replicas of x are identical (same x_1, same broadcast), so one
  * x is kept.
  * ------------------------------------------------------------------------- */
+/* The toy problem of Section V-A: gradient of ||A x - (x* + xi)||^2 is
+ * 2 A^T (A x - x* - xi). */
+void eao_toy_grad(int64_t d, int32_t N, const float *A, const float *x_star, const float *xi,
+                  const float *x, float *g, double *grad_sq)
+{
+    double *ax = (double *)malloc((size_t)d * sizeof(double));
+    double *res = (double *)malloc((size_t)d * sizeof(double));
+    for (int64_t k = 0; k < d; ++k) {
+        double s = 0.0;
+        for (int64_t j = 0; j < d; ++j) s += (double)A[k * d + j] * (double)x[j];
+        ax[k] = s;
+    }
+    for (int32_t i = 0; i < N; ++i) {
+        for (int64_t k = 0; k < d; ++k) res[k] = ax[k] - (double)x_star[k] - (double)xi[(int64_t)i * d + k];
+        for (int64_t j = 0; j < d; ++j) {
+            double s = 0.0;
+            for (int64_t k = 0; k < d; ++k) s += (double)A[k * d + j] * res[k];
+            g[(int64_t)i * d + j] = (float)(2.0 * s);
+        }
+    }
+    if (grad_sq) {
+        double tot = 0.0;
+        for (int64_t k = 0; k < d; ++k) res[k] = ax[k] - (double)x_star[k];
+        for (int64_t j = 0; j < d; ++j) {
+            double s = 0.0;
+            for (int64_t k = 0; k < d; ++k) s += (double)A[k * d + j] * res[k];
+            s = 2.0 * s;
+            tot += s * s;
+        }
+        *grad_sq = tot;
+    }
+    free(ax);
+    free(res);
+}
+
 /* Schedules: Assumption 2's theta_t = 1 - theta/T and alpha_t = alpha/sqrt(T);
  * Section V-B's decay of alpha by a constant factor every `period` steps. */
 int eao_schedule_at(const eao_schedule *s, float lr0, float beta2_0, int64_t t,

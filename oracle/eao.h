@@ -125,6 +125,19 @@ typedef struct {
 int eao_schedule_at(const eao_schedule *s, float lr0, float beta2_0, int64_t t,
                     float *lr, float *beta2);
 
+/* Gradients of the toy problem of Section V-A, f(x) = E_xi || A x - (x* + xi) ||^2,
+ * for N workers with noise draws xi_i (given):
+ *   res_i = A x - x* - xi_i            (A x summed over j in binary64, then the
+ *                                       two subtractions in binary64, in order)
+ *   g_i   = 2 A^T res_i                (summed over k in binary64, then x2,
+ *                                       rounded once to binary32)
+ * and, if grad_sq is not NULL, *grad_sq = || 2 A^T (A x - x*) ||^2 in binary64
+ * (the full gradient's squared norm, Figure 1's y-axis).  A is d x d,
+ * row-major; xi and g are [N][d].  Pinned by finite differences of the
+ * objective, the identity matrix case, and the noise-free consistency. */
+void eao_toy_grad(int64_t d, int32_t N, const float *A, const float *x_star, const float *xi,
+                  const float *x, float *g, double *grad_sq);
+
 /* One full round at step t (1-based) on the segment [n0, n0+len) of the
  * d-vector.  Arrays are segment-local:
  *   g, e_w            [N][len]   gradients; worker residuals (in/out)

@@ -68,6 +68,7 @@ def lib():
         L.eao_step.restype = C.c_int
         L.eao_schedule_at.argtypes = [C.POINTER(Schedule), C.c_float, C.c_float, C.c_int64, P, P]
         L.eao_schedule_at.restype = C.c_int
+        L.eao_toy_grad.argtypes = [C.c_int64, C.c_int32, P, P, P, P, P, P]
         _lib = L
     return _lib
 
@@ -168,6 +169,20 @@ def schedule_at(s: Schedule, lr0: float, beta2_0: float, t: int):
     if lib().eao_schedule_at(C.byref(s), lr0, beta2_0, t, _ptr(lr), _ptr(b2)) != 0:
         raise ValueError("invalid schedule")
     return lr[0], b2[0]
+
+
+def toy_grad(A: np.ndarray, x_star: np.ndarray, xi: np.ndarray, x: np.ndarray, want_norm: bool = True):
+    """Section V-A toy problem: g[N][d] = 2 A^T (A x - x* - xi_i) in binary32
+    and the full gradient's squared norm (binary64)."""
+    A = np.ascontiguousarray(A, np.float32)
+    d = A.shape[0]
+    xi = np.ascontiguousarray(xi, np.float32).reshape(-1, d)
+    N = xi.shape[0]
+    g = np.zeros((N, d), np.float32)
+    gs = np.zeros(1, np.float64)
+    lib().eao_toy_grad(d, N, _ptr(A), _ptr(np.ascontiguousarray(x_star, np.float32)), _ptr(xi),
+                       _ptr(np.ascontiguousarray(x, np.float32)), _ptr(g), _ptr(gs) if want_norm else None)
+    return g, float(gs[0])
 
 
 def adam_update(lr: float, m: float, v: float) -> float:

@@ -645,3 +645,60 @@ def test_paper_toy_error_feedback_ablation(seed):
     assert full < g0 / 10 and com1 < g0 / 10 and com2 < g0 / 10   # ||grad F||^2 decreases
     assert com1 < 0.5 * com1_err       # Figure 2: with Example 1, error feedback helps
     assert com2 < 1.05 * full          # Example 2 is about as good as full precision
+
+
+# ---------------------------------------------------------------------------
+# Section V-A toy problem: the oracle's gradient against finite differences
+# of the objective, special cases and the noise-free consistency.
+# ---------------------------------------------------------------------------
+def _toy_inputs(d, N, seed):
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((d, d)).astype(np.float32)
+    xs = (rng.standard_normal(d) * math.sqrt(0.1)).astype(np.float32)
+    xi = (rng.standard_normal((N, d)) * math.sqrt(0.1)).astype(np.float32)
+    x = rng.standard_normal(d).astype(np.float32)
+    return A, xs, xi, x
+
+
+def _objective(A, xs, xi_i, x):
+    """||A x - (x* + xi)||^2 by plain loops in binary64."""
+    d = len(x)
+    tot = 0.0
+    for k in range(d):
+        r = sum(float(A[k, j]) * float(x[j]) for j in range(d)) - float(xs[k]) - float(xi_i[k])
+        tot += r * r
+    return tot
+
+
+@pytest.mark.parametrize("d,N,seed", [(5, 2, 0), (9, 3, 1)])
+def test_toy_grad_matches_finite_differences(d, N, seed):
+    A, xs, xi, x = _toy_inputs(d, N, seed)
+    g, _ = O.toy_grad(A, xs, xi, x)
+    h = 1e-3
+    for i in range(N):
+        for j in range(d):
+            xp, xm = x.astype(np.float64).copy(), x.astype(np.float64).copy()
+            xp[j] += h
+            xm[j] -= h
+            # the objective is quadratic: central differences are exact up to rounding
+            fd = (_objective(A, xs, xi[i], xp) - _objective(A, xs, xi[i], xm)) / (2 * h)
+            assert abs(g[i, j] - fd) <= 1e-6 * (abs(fd) + 1.0), (i, j, g[i, j], fd)
+
+
+def test_toy_grad_identity_matrix_and_noise_free_norm():
+    d, N = 64, 4
+    _, xs, xi, x = _toy_inputs(d, N, 3)
+    A = np.eye(d, dtype=np.float32)
+    g, gsq = O.toy_grad(A, xs, xi, x)
+    want = (2.0 * (x.astype(np.float64) - xs - xi)).astype(np.float32)
+    assert np.array_equal(g, want)
+    assert gsq == pytest.approx(float(np.sum((2.0 * (x.astype(np.float64) - xs)) ** 2)), rel=1e-12)
+    # a general matrix: the squared norm is that of the noise-free gradient,
+    # and every worker's gradient differs from it by -2 A^T xi_i
+    A, xs, xi, x = _toy_inputs(40, 3, 4)
+    g, gsq = O.toy_grad(A, xs, xi, x)
+    g0, gsq0 = O.toy_grad(A, xs, np.zeros((1, 40), np.float32), x)
+    assert gsq == gsq0
+    assert gsq == pytest.approx(float(np.sum(g0.astype(np.float64) ** 2)), rel=1e-6)
+    lin = g0[0].astype(np.float64) - 2.0 * (xi.astype(np.float64) @ A.astype(np.float64))
+    assert np.allclose(g, lin, rtol=1e-5, atol=1e-4)
