@@ -118,12 +118,70 @@ def cpu_baseline(E, w, cfg, rb, sample):
                       f"{dt:.2f} s"}
 
 
+def paper_toy(args, E, allocate, init_state):
+    """Section V-A on the device: per step, the N workers' gradients
+    2 A^T (A x - x* - xi_i) at the current x (ea_toy_grad), then one round
+    (Example 2 with k = -17, K = -11, Adam at the workers, beta = 0.9,
+    theta = 0.99, lr = 1e-4).  The noise draws of all steps are generated
+    before the timed region.  The problem lives in cache: the step is bound by
+    launch latency, so the roofline fraction is reported for completeness."""
+    import torch
+    toy = W.PAPER_TOY
+    d, N = toy["d"], toy["N"]
+    q = E.Quant(kind=E.EA_Q_POW2, pow2_kmin=-17, pow2_kmax=-11, error_feedback=1)
+    cfg = E.Config(d=d, N=N, placement=E.EA_ADAM_AT_WORKER, beta1=toy["beta1"], beta2=toy["beta2"], lr=1e-4,
+                   eps=1e-8, seed=7, qw=q, qs=q)
+    rb = allocate(cfg)
+    init_state(cfg, rb)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7)
+    A = torch.randn((d, d), generator=gen, device="cuda")
+    xs = torch.randn(d, generator=gen, device="cuda") * toy["x_star_var"] ** 0.5
+    total = args.warmup + args.steps
+    xi = torch.randn((total, N, d), generator=gen, device="cuda") * toy["xi_var"] ** 0.5
+    gsq = torch.zeros(total, dtype=torch.float64, device="cuda")
+    ws = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    step_args = rb.step_args()
+
+    def one(k):
+        E.ea_toy_grad(d, N, A, xs, xi[k], rb.x, rb.g, gsq[k:k + 1], ws, stream=stream)
+        E.ea_step(cfg, k + 1, **step_args, stream=stream)
+
+    for k in range(args.warmup):
+        one(k)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(args.warmup, total):
+        one(k)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    alg = algorithmic_bytes(E, cfg) + 2 * 4 * d * d      # the round + A read twice by the gradient
+    g = gsq.cpu().numpy()
+    line = {
+        "metric": "Section V-A toy problem, steps per second (gradient producer + round)",
+        "value": round(1e3 / ms, 1), "unit": "steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "paper_toy d=500 N=10 Example 2, Adam at the workers", "d": d, "N": N},
+        "roofline": {"bound": "hbm", "achieved": round(alg / (ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(alg / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 5), "traffic": None,
+                     "kernel": "toy gradient kernels + step_kernel (cache-resident; launch-bound)"},
+        "grad_sq_first_last": [float(g[0]), float(g[-1])],
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="bert", choices=list(W.WORKLOADS))
+    ap.add_argument("--workload", default="bert", choices=list(W.WORKLOADS) + ["paper_toy"],
+                    help="paper_toy: Section V-A's problem (d = 500, N = 10, Example 2, Adam at the "
+                         "workers), each step = ea_toy_grad at the current x + one round")
     ap.add_argument("--call", default="step", choices=["step", "scheduled", "graph"],
                     help="time ea_step (default), ea_step_scheduled with the step on the device and a "
                          "Section V-B step-decay schedule, or that call captured once in a HIP graph and "
@@ -158,6 +216,9 @@ def main():
 
     import paper_2205_14473_amd as E
     from paper_2205_14473_amd.state import allocate, init_state
+
+    if args.workload == "paper_toy":
+        return paper_toy(args, E, allocate, init_state)
 
     w = W.WORKLOADS[args.workload]
     placement = E.EA_ADAM_AT_SERVER if args.placement == "server" else E.EA_ADAM_AT_WORKER

@@ -241,6 +241,23 @@ int ea_run(const ea_config_t *c, const ea_schedule_t *s, int64_t t0, int64_t ste
            float *x, uint64_t *wcodes, float *wscales, uint64_t *scodes, float *sscales, void *workspace,
            void *stream);
 
+/* ---- the toy problem of Section V-A -------------------------------------- */
+
+/* Device workspace (bytes) of ea_toy_grad for dimension d. */
+int64_t ea_toy_workspace_bytes(int64_t d);
+
+/* Gradients of f(x) = E_xi || A x - (x* + xi) ||^2 (Section V-A) for N
+ * workers: g_i = 2 A^T (A x - x* - xi_i), and, if grad_sq is not NULL, the
+ * squared norm of the full gradient 2 A^T (A x - x*) (Figure 1's y-axis).
+ *   A (device, d*d, row-major), x_star, x (device, d), xi (device, N*d: the
+ *   workers' noise draws, supplied by the caller), g (device, N*d, write),
+ *   grad_sq (device, one double, write; NULL to skip), workspace (device,
+ *   ea_toy_workspace_bytes(d) bytes, 8-byte aligned).
+ *   Products are summed in binary64 and each g_i rounded once to binary32.
+ *   1 <= d <= 65536, 1 <= N <= 1024. */
+int ea_toy_grad(int64_t d, int32_t N, const float *A, const float *x_star, const float *xi, const float *x,
+                float *g, double *grad_sq, void *workspace, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -72,6 +72,8 @@ def _load():
         "ea_schedule_at": (C.c_int, [CP, SP, I64, P, P]),
         "ea_step_scheduled": (C.c_int, [CP, SP] + [P] * 15),
         "ea_run": (C.c_int, [CP, SP, I64, I64, P, I64] + [P] * 13),
+        "ea_toy_workspace_bytes": (I64, [I64]),
+        "ea_toy_grad": (C.c_int, [I64, I32] + [P] * 8),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -220,3 +222,14 @@ def ea_run(cfg, sched, t0, steps, g, g_step_stride, e_w, m_w, v_w, m, v, e_s, x,
                              _ptr(m_w, f), _ptr(v_w, f), _ptr(m, f), _ptr(v, f), _ptr(e_s, f), _ptr(x, f),
                              _ptr(wcodes, u), _ptr(wscales, f), _ptr(scodes, u), _ptr(sscales, f),
                              _ptr(workspace), _stream(stream)))
+
+
+def ea_toy_workspace_bytes(d):
+    return _check(lib.ea_toy_workspace_bytes(d))
+
+
+def ea_toy_grad(d, N, A, x_star, xi, x, g, grad_sq, workspace, stream=None):
+    import torch
+    f = _f32()
+    return _check(lib.ea_toy_grad(d, N, _ptr(A, f), _ptr(x_star, f), _ptr(xi, f), _ptr(x, f), _ptr(g, f),
+                                  _ptr(grad_sq, torch.float64), _ptr(workspace), _stream(stream)))

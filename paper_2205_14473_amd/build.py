@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libea.so")
-SOURCES = [os.path.join(CSRC, "ea_kernels.hip"), os.path.join(CSRC, "ea_api.cpp")]
+SOURCES = [os.path.join(CSRC, f) for f in ("ea_kernels.hip", "ea_toy.hip", "ea_api.cpp")]
 HEADERS = [os.path.join(CSRC, f) for f in ("ea_device.hpp", "ea_launch.hpp")] + [os.path.join(ROOT, "include", "ea.h")]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

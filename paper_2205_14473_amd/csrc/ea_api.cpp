@@ -598,4 +598,30 @@ int ea_run(const ea_config_t* c, const ea_schedule_t* s, int64_t t0, int64_t ste
     return ok();
 }
 
+int64_t ea_toy_workspace_bytes(int64_t d)
+{
+    if (d < 1 || d > ea::kToyMaxD) return fail(EA_ERR_ARG, "toy gradient needs 1 <= d <= %lld (got %lld)",
+                                               (long long)ea::kToyMaxD, (long long)d);
+    return ea::toy_workspace_bytes(d);
+}
+
+int ea_toy_grad(int64_t d, int32_t N, const float* A, const float* x_star, const float* xi, const float* x,
+                float* g, double* grad_sq, void* workspace, void* stream)
+{
+    if (d < 1 || d > ea::kToyMaxD) return fail(EA_ERR_ARG, "toy gradient needs 1 <= d <= %lld (got %lld)",
+                                               (long long)ea::kToyMaxD, (long long)d);
+    if (N < 1 || N > 1024) return fail(EA_ERR_ARG, "N must be in [1, 1024] (got %d)", N);
+    PtrCheck pc;
+    pc.need(A, true, 4, "A");
+    pc.need(x_star, true, 4, "x_star");
+    pc.need(xi, true, 4, "xi");
+    pc.need(x, true, 4, "x");
+    pc.need(g, true, 4, "g");
+    pc.need(grad_sq, false, 8, "grad_sq");
+    pc.need(workspace, true, 8, "workspace");
+    if (pc.rc) return pc.rc;
+    return hip_status(ea::launch_toy_grad(d, N, A, x_star, xi, x, g, grad_sq, workspace, (hipStream_t)stream),
+                      "ea_toy_grad");
+}
+
 }  // extern "C"

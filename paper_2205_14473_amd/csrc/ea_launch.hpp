@@ -65,5 +65,12 @@ hipError_t launch_apply(const StepArgs& a, int C, bool vec, hipStream_t s);
 hipError_t launch_fill(float* p, int64_t n, float value, hipStream_t s);
 // t_dev[0] <- t_dev[0] + 1 (after the kernels of a round that read it).
 hipError_t launch_advance(uint32_t* t_dev, hipStream_t s);
+// Toy problem of Section V-A: g = 2 A^T (A x - x* - xi_i) for N workers and
+// the noise-free gradient's squared norm.  The workspace holds the residual
+// and per-block partial norms (toy_workspace_bytes).
+constexpr int64_t kToyMaxD = 65536;
+int64_t toy_workspace_bytes(int64_t d);
+hipError_t launch_toy_grad(int64_t d, int32_t N, const float* A, const float* xs, const float* xi, const float* x,
+                           float* g, double* grad_sq, void* workspace, hipStream_t s);
 
 }  // namespace ea

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(E):
     names = _declared()
-    assert len(names) == 16, names
+    assert len(names) == 18, names
     for n in names:
         assert hasattr(E.lib, n), f"{n} declared in include/ea.h but not exported"
 
@@ -185,3 +185,24 @@ def test_scheduled_calls_rejected_before_device_work(E):
     assert E.lib.ea_run(sb(c), sb(bad), 1, 3, g0, 0, *rest) == E.EA_ERR_ARG
     assert E.lib.ea_run(sb(c), sb(s), 1, 3, None, 0, *rest) == E.EA_ERR_ARG
     assert E.lib.ea_run(sb(c), sb(s), 1, 0, g0, 0, *rest) == E.EA_OK   # nothing to do
+
+
+def test_toy_grad_rejected_before_device_work(E):
+    torch = pytest.importorskip("torch")
+    if torch.cuda.device_count() > 0:
+        pytest.skip("bogus-pointer rejection test runs on GPU-less hosts only")
+    P = ctypes.c_void_p
+    p = [P(4096 * (k + 1)) for k in range(5)]     # A, x_star, xi, x, g
+    ws = P(1 << 20)
+    assert E.lib.ea_toy_grad(0, 2, *p, None, ws, None) == E.EA_ERR_ARG
+    assert E.lib.ea_toy_grad(65537, 2, *p, None, ws, None) == E.EA_ERR_ARG
+    assert E.lib.ea_toy_grad(500, 0, *p, None, ws, None) == E.EA_ERR_ARG
+    assert E.lib.ea_toy_grad(500, 1025, *p, None, ws, None) == E.EA_ERR_ARG
+    assert E.lib.ea_toy_grad(500, 10, None, *p[1:], None, ws, None) == E.EA_ERR_ARG
+    assert E.lib.ea_toy_grad(500, 10, *p[:4], P(4098), None, ws, None) == E.EA_ERR_ALIGN
+    assert E.lib.ea_toy_grad(500, 10, *p, P(4100), ws, None) == E.EA_ERR_ALIGN
+    assert E.lib.ea_toy_grad(500, 10, *p, None, None, None) == E.EA_ERR_ARG
+    assert E.lib.ea_toy_grad(500, 10, *p, None, P(4100), None) == E.EA_ERR_ALIGN
+    assert E.ea_toy_workspace_bytes(500) == 8 * (500 + 8)
+    with pytest.raises(E.EAError):
+        E.ea_toy_workspace_bytes(0)

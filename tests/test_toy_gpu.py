@@ -1,0 +1,102 @@
+"""GPU parity of the Section V-A toy problem's gradient producer
+(ea_toy_grad) against the oracle, and Figure 1's setting run on the device:
+each step the workers' gradients come from ea_toy_grad at the current x and
+feed the round, while the oracle runs the same steps."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU-only host
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2205_14473_amd as E  # noqa: E402
+from parity_util import Pair, qfields  # noqa: E402
+
+
+def _inputs(d, N, seed):
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((d, d)).astype(np.float32)
+    xs = (rng.standard_normal(d) * math.sqrt(0.1)).astype(np.float32)
+    xi = (rng.standard_normal((N, d)) * math.sqrt(0.1)).astype(np.float32)
+    x = rng.standard_normal(d).astype(np.float32)
+    return A, xs, xi, x
+
+
+def _gpu_grad(A, xs, xi, x):
+    d, N = A.shape[0], xi.shape[0]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    g = torch.empty((N, d), dtype=torch.float32, device="cuda")
+    gs = torch.zeros(1, dtype=torch.float64, device="cuda")
+    ws = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+    E.ea_toy_grad(d, N, dev(A), dev(xs), dev(xi), dev(x), g, gs, ws)
+    torch.cuda.synchronize()
+    return g.cpu().numpy(), float(gs.item())
+
+
+def _check(got, want, gs_got, gs_want):
+    # binary64 sums in another order: the binary32 results agree to the
+    # rounding of the last place
+    scale = np.max(np.abs(want))
+    assert np.all(np.abs(got - want) <= 1e-6 * np.abs(want) + 1e-9 * scale)
+    assert gs_got == pytest.approx(gs_want, rel=1e-12)
+
+
+@pytest.mark.parametrize("d,N,seed", [(1, 1, 0), (7, 3, 1), (64, 8, 2), (65, 9, 8), (500, 10, 3), (1000, 17, 4),
+                                      (4099, 2, 5), (8192, 1, 6)])
+def test_toy_grad_matches_oracle(d, N, seed):
+    A, xs, xi, x = _inputs(d, N, seed)
+    g, gs = _gpu_grad(A, xs, xi, x)
+    go, gso = O.toy_grad(A, xs, xi, x)
+    _check(g, go, gs, gso)
+    print(f"\n[toy] d={d} N={N}: exact entries {np.mean(g == go):.6f}", flush=True)
+
+
+def test_toy_grad_without_norm():
+    A, xs, xi, x = _inputs(300, 4, 7)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    g = torch.empty((4, 300), dtype=torch.float32, device="cuda")
+    ws = torch.empty(E.ea_toy_workspace_bytes(300), dtype=torch.uint8, device="cuda")
+    E.ea_toy_grad(300, 4, dev(A), dev(xs), dev(xi), dev(x), g, None, ws)
+    torch.cuda.synchronize()
+    go, _ = O.toy_grad(A, xs, xi, x, want_norm=False)
+    _check(g.cpu().numpy(), go, 0.0, 0.0)
+
+
+@pytest.mark.parametrize("example", ["ex1", "ex2"])
+def test_figure1_setting_on_device(example):
+    """Section V-A: d = 500, 10 workers, Adam at the workers, beta = 0.9,
+    theta = 0.99, Example 1 (k = 1) or Example 2 (k = -17, K = -11); the
+    gradients come from ea_toy_grad at the GPU's x each step."""
+    d, N, T, lr = 500, 10, 40, 1e-4
+    rng = np.random.default_rng(21)
+    A = rng.standard_normal((d, d)).astype(np.float32)
+    xs = (rng.standard_normal(d) * math.sqrt(0.1)).astype(np.float32)
+    if example == "ex1":
+        q = qfields(O.Q_DET_UNIFORM, 2, bucket=0)
+    else:
+        q = qfields(O.Q_POW2, kmin=-17, kmax=-11)
+    pair = Pair(d, N, q, q, O.ADAM_AT_WORKER, seed=21, beta1=0.9, beta2=0.99, lr=lr)
+    A_d, xs_d = torch.from_numpy(A).cuda(), torch.from_numpy(xs).cuda()
+    g_d = torch.empty((N, d), dtype=torch.float32, device="cuda")
+    gs_d = torch.zeros(1, dtype=torch.float64, device="cuda")
+    ws = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+    norms = []
+    for t in range(1, T + 1):
+        xi = (rng.standard_normal((N, d)) * math.sqrt(0.1)).astype(np.float32)
+        xi_d = torch.from_numpy(xi).cuda()
+        E.ea_toy_grad(d, N, A_d, xs_d, xi_d, pair.rb.x, g_d, gs_d, ws)
+        torch.cuda.synchronize()
+        go, gso = O.toy_grad(A, xs, xi, pair.ost.x)
+        _check(g_d.cpu().numpy(), go, float(gs_d.item()), gso)
+        norms.append(gso)
+        pair.step(t, go)        # the round on the same gradients, both sides
+    pair.check_tie_budget()
+    assert norms[-1] < norms[0]
+    print(f"\n[toy] figure-1 setting {example}: |grad F|^2 {norms[0]:.4g} -> {norms[-1]:.4g}; {pair.stats}",
+          flush=True)
