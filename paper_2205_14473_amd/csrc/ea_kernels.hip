@@ -1,18 +1,21 @@
 // ea_kernels.hip -- HIP kernels of one Efficient-Adam round for gfx950.
 //
-// Work decomposition: one wave64 owns one tile of C chunks (C*256 elements);
-// a block holds 4 independent waves.  Bucket norms are reduced inside the
-// wave (no LDS, no barrier); codes are bit-plane packed with one ballot per
-// 64-element plane word.  The fused step streams the N workers of a tile in
-// ascending worker order (the next worker's rows are loaded while the
-// current one is quantized), keeps the dequantized sum in registers, and
-// runs the server's Adam, quantization and the parameter update on the same
-// tile (Algorithms 1-2, Section IV).
+// Work decomposition.  A tile is C chunks of 256 elements; a wave64 holds a
+// tile of one vector, four consecutive elements per lane.  Bucket norms are
+// reduced inside the wave (no LDS, no barrier); codes are bit-plane packed
+// with one ballot per 64-element plane word.
+//
+// The fused round (step_kernel) gives a block K consecutive tiles and one
+// wave per worker: each wave compresses its worker on the block's tiles and
+// hands the dequantized values over through LDS; then wave k adds the
+// handoffs of tile k in ascending worker order and runs the server's Adam,
+// quantization and the update of x on that tile (Algorithms 1-2, Section IV).
+// The split calls use blocks of 4 independent waves, one tile each.
 //
 // Every kernel is a template over the quantizer traits of both sides and the
 // Adam placement: QRt / placement -1 give the generic kernels used for any
 // configuration, QCt<...> the specialized ones for common shapes.  Tiles
-// that lie wholly inside d take a path without per-element bounds checks.
+// that lie wholly inside d go to kernels without per-element bounds checks.
 #include "ea_launch.hpp"
 
 namespace ea {
