@@ -90,9 +90,17 @@ int32_t eao_code_bits(const eao_quant *q)
     case EAO_Q_POW2:
         if (q->pow2_kmin < -126 || q->pow2_kmax > 127 || q->pow2_kmin >= q->pow2_kmax) return -1;
         return pow2_bits(q->pow2_kmin, q->pow2_kmax);
+    case EAO_Q_TOPK:
+    case EAO_Q_RANDK:
+        return q->keep >= 1 ? 1 : -1;   /* the code is the kept flag */
     default:
         return -1;
     }
+}
+
+static int is_sparse(const eao_quant *q)
+{
+    return q->kind == EAO_Q_TOPK || q->kind == EAO_Q_RANDK;
 }
 
 static int has_scales(const eao_quant *q)
@@ -109,8 +117,9 @@ int64_t eao_bucket_len(const eao_quant *q, int64_t d)
 
 int64_t eao_num_scales(const eao_quant *q, int64_t d, int64_t len)
 {
-    if (!has_scales(q)) return 0;
     const int64_t B = eao_bucket_len(q, d);
+    if (is_sparse(q)) return (len + B - 1) / B * q->keep;
+    if (!has_scales(q)) return 0;
     return (len + B - 1) / B;
 }
 
@@ -261,6 +270,56 @@ static void q_pow2(const eao_quant *q, int64_t n, const float *p, uint32_t *code
     }
 }
 
+/* Definition 3 sparsifiers (TOPK, RANDK; see eao.h for the ranking).  The
+ * ranking is a sort of (key, index) pairs, larger key first, lower index
+ * first among equal keys; the first min(keep, n) are kept. */
+typedef struct {
+    uint32_t key;
+    int64_t idx;
+} eao_ranked;
+
+static int by_rank(const void *a, const void *b)
+{
+    const eao_ranked *x = (const eao_ranked *)a, *y = (const eao_ranked *)b;
+    if (x->key != y->key) return x->key > y->key ? -1 : 1;
+    return x->idx < y->idx ? -1 : (x->idx > y->idx ? 1 : 0);
+}
+
+static uint32_t magnitude_key(float x)
+{
+    uint32_t b;
+    memcpy(&b, &x, sizeof b);
+    return b & 0x7FFFFFFFu;
+}
+
+static int q_sparse(const eao_quant *q, int64_t n, const float *p, const float *u,
+                    uint32_t *code, float *deq, float *vals)
+{
+    eao_ranked *r = (eao_ranked *)malloc((size_t)n * sizeof(eao_ranked));
+    if (!r) return -1;
+    for (int64_t j = 0; j < n; ++j) {
+        /* u = w * 2^-24 for a 24-bit integer w, so u * 2^24 is w exactly. */
+        r[j].key = q->kind == EAO_Q_TOPK ? magnitude_key(p[j]) : (uint32_t)(u[j] * 16777216.0f);
+        r[j].idx = j;
+    }
+    qsort(r, (size_t)n, sizeof(eao_ranked), by_rank);
+    const int64_t k = q->keep < n ? q->keep : n;
+    for (int64_t j = 0; j < n; ++j) code[j] = 0;
+    for (int64_t i = 0; i < k; ++i) code[r[i].idx] = 1;
+    free(r);
+    int64_t slot = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        if (code[j]) {
+            deq[j] = p[j];
+            vals[slot++] = p[j];
+        } else {
+            deq[j] = 0.0f;
+        }
+    }
+    for (; slot < q->keep; ++slot) vals[slot] = 0.0f;
+    return 0;
+}
+
 /* Full-precision communication ("Ours_full" in Table 2): the code is the
  * binary32 bit pattern itself. */
 static void q_none(int64_t n, const float *p, uint32_t *code, float *deq)
@@ -277,7 +336,7 @@ int eao_quantize(const eao_quant *q, int64_t d, int64_t len, const float *p,
     if (eao_code_bits(q) < 0) return -1;
     if (q->kind == EAO_Q_STOCH_UNIFORM && q->scale != EAO_SCALE_L2 && q->scale != EAO_SCALE_MAX)
         return -1;
-    if (q->kind == EAO_Q_STOCH_UNIFORM && u == NULL) return -1;
+    if ((q->kind == EAO_Q_STOCH_UNIFORM || q->kind == EAO_Q_RANDK) && u == NULL) return -1;
     if (q->kind == EAO_Q_NONE) { q_none(len, p, code, deq); return 0; }
     if (q->kind == EAO_Q_POW2) { q_pow2(q, len, p, code, deq); return 0; }
     const int64_t B = eao_bucket_len(q, d);
@@ -293,6 +352,11 @@ int eao_quantize(const eao_quant *q, int64_t d, int64_t len, const float *p,
         case EAO_Q_DET_UNIFORM:
             q_det_uniform(q, n, p + b0, code + b0, deq + b0, &scales[bi]);
             break;
+        case EAO_Q_TOPK:
+        case EAO_Q_RANDK:
+            if (q_sparse(q, n, p + b0, u ? u + b0 : NULL, code + b0, deq + b0, scales + bi * q->keep))
+                return -1;
+            break;
         default:
             return -1;
         }
@@ -306,6 +370,16 @@ int eao_dequantize(const eao_quant *q, int64_t d, int64_t len, const uint32_t *c
     const int32_t b = eao_code_bits(q);
     if (b < 0) return -1;
     const int64_t B = eao_bucket_len(q, d);
+    if (is_sparse(q)) {
+        /* Kept elements take the bucket's values in index order. */
+        for (int64_t b0 = 0, bi = 0; b0 < len; b0 += B, ++bi) {
+            const int64_t n = (len - b0 < B) ? (len - b0) : B;
+            int64_t slot = 0;
+            for (int64_t j = 0; j < n; ++j)
+                deq[b0 + j] = code[b0 + j] ? scales[bi * q->keep + slot++] : 0.0f;
+        }
+        return 0;
+    }
     for (int64_t j = 0; j < len; ++j) {
         const uint32_t c = code[j];
         switch (q->kind) {
@@ -492,7 +566,10 @@ static int check_segment(const eao_quant *q, int64_t d, int64_t n0, int64_t len)
     return 0;
 }
 
-static int needs_draws(const eao_quant *q) { return q->kind == EAO_Q_STOCH_UNIFORM; }
+static int needs_draws(const eao_quant *q)
+{
+    return q->kind == EAO_Q_STOCH_UNIFORM || q->kind == EAO_Q_RANDK;
+}
 
 int eao_step(const eao_config *c, uint32_t t, int64_t n0, int64_t len,
              const float *g, float *e_w, float *m_w, float *v_w,
@@ -537,7 +614,10 @@ int eao_step(const eao_config *c, uint32_t t, int64_t n0, int64_t len,
             for (int64_t n = 0; n < len; ++n) p[n] = gi[n] + ei[n];
         }
         if (needs_draws(&c->qw)) eao_uniforms(c->seed, t, (uint32_t)i, n0, len, u);
-        eao_quantize(&c->qw, d, len, p, u, code, deq, wscales + (int64_t)i * scales_w);
+        if (eao_quantize(&c->qw, d, len, p, u, code, deq, wscales + (int64_t)i * scales_w)) {
+            free(p); free(u); free(deq); free(acc); free(code);
+            return -1;
+        }
         eao_pack(bw, len, code, wcodes + (int64_t)i * words_w);
         for (int64_t n = 0; n < len; ++n) {
             ei[n] = c->qw.error_feedback ? p[n] - deq[n] : 0.0f;
@@ -557,7 +637,10 @@ int eao_step(const eao_config *c, uint32_t t, int64_t n0, int64_t len,
         p[n] = a + e_s[n];
     }
     if (needs_draws(&c->qs)) eao_uniforms(c->seed, t, 0xFFFFFFFFu, n0, len, u);
-    eao_quantize(&c->qs, d, len, p, u, code, deq, sscales);
+    if (eao_quantize(&c->qs, d, len, p, u, code, deq, sscales)) {
+        free(p); free(u); free(deq); free(acc); free(code);
+        return -1;
+    }
     eao_pack(bs, len, code, scodes);
     for (int64_t n = 0; n < len; ++n) {
         e_s[n] = c->qs.error_feedback ? p[n] - deq[n] : 0.0f;

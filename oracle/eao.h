@@ -27,7 +27,7 @@ extern "C" {
 #endif
 
 enum { EAO_Q_NONE = 0, EAO_Q_SCALED_SIGN = 1, EAO_Q_STOCH_UNIFORM = 2,
-       EAO_Q_DET_UNIFORM = 3, EAO_Q_POW2 = 4 };
+       EAO_Q_DET_UNIFORM = 3, EAO_Q_POW2 = 4, EAO_Q_TOPK = 5, EAO_Q_RANDK = 6 };
 enum { EAO_SCALE_L1 = 0, EAO_SCALE_L2 = 1, EAO_SCALE_MAX = 2 };
 enum { EAO_ADAM_AT_SERVER = 0, EAO_ADAM_AT_WORKER = 1 };
 
@@ -40,7 +40,25 @@ typedef struct {
     int64_t bucket;          /* elements per scale bucket; 0 or >= d: one bucket */
     int32_t pow2_kmin;       /* Example 2: M = {2^kmin, ..., 2^kmax}            */
     int32_t pow2_kmax;
+    int32_t keep;            /* TOPK, RANDK: elements kept per bucket, >= 1     */
+    int32_t reserved;        /* 0                                               */
 } eao_quant;
+
+/* Definition 3 compressors (the sparsifiers of the works it cites): in each
+ * bucket of n elements the k = min(keep, n) highest-ranked elements are kept
+ * and the others sent as 0, which meets ||x - Q(x)||^2 <= (1 - k/n) ||x||^2
+ * for TOPK (and in expectation, with equality, for RANDK).  Ranking is by a
+ * 32-bit key, larger first, equal keys by lower index:
+ *   TOPK   key = the binary32 pattern of x with the sign bit cleared, an order
+ *          that equals the order of |x| on all non-NaN values (NaN ranks above
+ *          infinity);
+ *   RANDK  key = u * 2^24 for the element's uniform draw u (the 24-bit word
+ *          the draw is made of), so the kept set is the k largest of n
+ *          independent uniform keys: a uniformly random k-subset up to equal
+ *          keys.
+ * Code 1 marks a kept element.  The message's value array holds `keep`
+ * binary32 numbers per bucket: the kept values in index order, then zeros
+ * (only a last bucket shorter than keep has any). */
 
 typedef struct {
     int64_t d;               /* parameters                                      */
@@ -70,15 +88,17 @@ void eao_uniforms(uint64_t seed, uint32_t t, uint32_t stream,
 int32_t eao_code_bits(const eao_quant *q);
 /* Bucket length used for a vector of d elements. */
 int64_t eao_bucket_len(const eao_quant *q, int64_t d);
-/* Number of per-bucket scales for a segment of len elements (0: none). */
+/* Number of per-bucket scales for a segment of len elements (0: none); for
+ * TOPK and RANDK the number of values, keep per bucket. */
 int64_t eao_num_scales(const eao_quant *q, int64_t d, int64_t len);
 /* Number of 64-bit message words for a segment of len elements. */
 int64_t eao_msg_words(const eao_quant *q, int64_t len);
 
 /* Quantize a segment p[0..len) that starts on a bucket boundary of a vector
  * of d elements.  u[] holds one uniform draw per element (read only by
- * STOCH_UNIFORM; may be NULL otherwise).  Writes one integer code and one
- * dequantized value per element, and one scale per bucket.  Returns 0, or -1
+ * STOCH_UNIFORM and RANDK; may be NULL otherwise).  Writes one integer code and
+ * one dequantized value per element, and one scale per bucket (TOPK, RANDK:
+ * keep values per bucket).  Returns 0, or -1
  * on an invalid description. */
 int eao_quantize(const eao_quant *q, int64_t d, int64_t len, const float *p,
                  const float *u, uint32_t *code, float *deq, float *scales);

@@ -12,7 +12,7 @@ import numpy as np
 
 from .build import ensure_built
 
-Q_NONE, Q_SCALED_SIGN, Q_STOCH_UNIFORM, Q_DET_UNIFORM, Q_POW2 = 0, 1, 2, 3, 4
+Q_NONE, Q_SCALED_SIGN, Q_STOCH_UNIFORM, Q_DET_UNIFORM, Q_POW2, Q_TOPK, Q_RANDK = 0, 1, 2, 3, 4, 5, 6
 SCALE_L1, SCALE_L2, SCALE_MAX = 0, 1, 2
 ADAM_AT_SERVER, ADAM_AT_WORKER = 0, 1
 SCHED_CONSTANT, SCHED_ASSUMPTION2, SCHED_STEP_DECAY = 0, 1, 2
@@ -21,7 +21,8 @@ SCHED_CONSTANT, SCHED_ASSUMPTION2, SCHED_STEP_DECAY = 0, 1, 2
 class Quant(C.Structure):
     _fields_ = [("kind", C.c_int32), ("scale", C.c_int32), ("bits", C.c_int32),
                 ("error_feedback", C.c_int32), ("bucket", C.c_int64),
-                ("pow2_kmin", C.c_int32), ("pow2_kmax", C.c_int32)]
+                ("pow2_kmin", C.c_int32), ("pow2_kmax", C.c_int32), ("keep", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class Config(C.Structure):
@@ -35,7 +36,7 @@ class Schedule(C.Structure):
                 ("T", C.c_int64), ("period", C.c_int64)]
 
 
-assert C.sizeof(Quant) == 32 and C.sizeof(Config) == 104 and C.sizeof(Schedule) == 32
+assert C.sizeof(Quant) == 40 and C.sizeof(Config) == 120 and C.sizeof(Schedule) == 32
 
 _lib = None
 

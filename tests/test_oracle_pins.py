@@ -499,6 +499,10 @@ CASES = [
     ("ex2-worker", O.ADAM_AT_WORKER, q_(O.Q_POW2, kmin=-17, kmax=-11), q_(O.Q_POW2, kmin=-17, kmax=-11)),
     ("stoch2-worker", O.ADAM_AT_WORKER, q_(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, bucket=256),
      q_(O.Q_SCALED_SIGN, 1, bucket=256)),
+    ("topk-server", O.ADAM_AT_SERVER, O.Quant(kind=O.Q_TOPK, keep=16, bucket=512, error_feedback=1),
+     O.Quant(kind=O.Q_TOPK, keep=8, bucket=256, error_feedback=1)),
+    ("randk-worker", O.ADAM_AT_WORKER, O.Quant(kind=O.Q_RANDK, keep=32, bucket=256, error_feedback=1),
+     O.Quant(kind=O.Q_TOPK, keep=64, bucket=1024, error_feedback=1)),
 ]
 
 
