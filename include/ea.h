@@ -28,6 +28,9 @@
  *           words hold the binary32 values themselves, element n in word n>>1
  *           (low half for even n); ea_msg_words() = ceil(d/2).
  *   scales  one binary32 per bucket, in bucket order (none for NONE, POW2).
+ *           TOPK, RANDK: `keep` binary32 values per bucket, in bucket order:
+ *           the kept values in element order, then zeros (only a last bucket
+ *           shorter than keep has any).
  *
  * Code tables
  *   SCALED_SIGN   b=1: code 1 = negative; value +-s, s = mean |p| of the bucket.
@@ -41,15 +44,26 @@
  *                 (j - kmin) for +-2^j, and the magnitude code kmax-kmin+1
  *                 for 0; b = 1 + ceil(log2(kmax-kmin+2)).
  *   NONE          the value itself ("32-bit floating point", Table 2).
+ *   TOPK, RANDK   Definition 3 compressors, b=1: code 1 marks a kept element,
+ *                 which is sent exactly; the others are sent as 0.  Each bucket
+ *                 of n elements keeps its min(keep, n) highest-ranked elements
+ *                 by a 32-bit key, larger first, equal keys by lower index:
+ *                 TOPK: the binary32 pattern with the sign cleared (the order
+ *                 of |p|; NaN ranks above infinity), so ||p - Q(p)||^2 <=
+ *                 (1 - keep/n) ||p||^2;  RANDK: the element's 24-bit draw
+ *                 word (see below), a uniformly random subset up to equal
+ *                 words.
  *
  * Buckets: `bucket` is 0 (one bucket over the whole vector), >= d (same), or
  * a multiple of 256 up to 2048; when both sides are bucketed, the larger of
- * the two buckets must be a multiple of the smaller.
+ * the two buckets must be a multiple of the smaller.  TOPK and RANDK need
+ * bucket 256, 512, 1024 or 2048 (a bucket >= d is one short bucket) and
+ * 1 <= keep <= bucket.
  *
  * Stochastic rounding draws: element n of stream s at step t uses word n&3
  * of Philox4x32-10 (Salmon et al., SC'11) applied to counter
  * {lo(n>>2), hi(n>>2), t, s} with key {lo(seed), hi(seed)}, as
- * u = (word>>8) * 2^-24.  Worker i uses stream i, the server 0xFFFFFFFF.
+ * u = (word>>8) * 2^-24; RANDK ranks by word>>8.  Worker i uses stream i, the server 0xFFFFFFFF.
  * Replaying a step t replays its draws.
  */
 #ifndef EA_H
@@ -72,6 +86,8 @@ extern "C" {
 #define EA_Q_STOCH_UNIFORM 2
 #define EA_Q_DET_UNIFORM 3
 #define EA_Q_POW2 4
+#define EA_Q_TOPK 5              /* Definition 3: top-k per bucket                 */
+#define EA_Q_RANDK 6             /* Definition 3: random-k per bucket              */
 
 #define EA_SCALE_L1 0
 #define EA_SCALE_L2 1
@@ -80,7 +96,7 @@ extern "C" {
 #define EA_ADAM_AT_SERVER 0      /* workers send Q_w(g + e); the server runs Adam  */
 #define EA_ADAM_AT_WORKER 1      /* Algorithms 1-2 as printed: workers run Adam    */
 
-/* One quantization mapping (Definition 1 / Definition 3). */
+/* One quantization mapping (Definition 1) or compressor (Definition 3). */
 typedef struct ea_quant {
     int32_t kind;            /* EA_Q_*                                                */
     int32_t scale;           /* STOCH_UNIFORM: EA_SCALE_L2 or EA_SCALE_MAX; else unused */
@@ -89,6 +105,8 @@ typedef struct ea_quant {
     int64_t bucket;          /* see "Buckets" above                                   */
     int32_t pow2_kmin;       /* POW2: Example 2's k, -126 <= kmin < kmax <= 127       */
     int32_t pow2_kmax;       /* POW2: Example 2's K                                   */
+    int32_t keep;            /* TOPK, RANDK: elements kept per bucket; else unused    */
+    int32_t reserved;        /* must be 0                                             */
 } ea_quant_t;
 
 /* Arguments of the round, following the paper's statement of the problem. */
@@ -111,7 +129,8 @@ typedef struct ea_config {
 int32_t ea_code_bits(const ea_quant_t *q);
 /* uint64 words of one message for a d-vector (see "Wire format"). */
 int64_t ea_msg_words(const ea_quant_t *q, int64_t d);
-/* binary32 scales of one message (0 for NONE and POW2). */
+/* binary32 scales of one message (0 for NONE and POW2; TOPK, RANDK: keep
+ * values per bucket). */
 int64_t ea_msg_scales(const ea_quant_t *q, int64_t d);
 /* Payload bits of one message: d*b plus 32 per scale (the communication
  * cost counted in Corollary 1 and on the x-axis of Figures 1, 3, 6). */

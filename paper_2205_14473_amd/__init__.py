@@ -10,7 +10,7 @@ exists; using a name with no library built raises ImportError.
 """
 _EXPORTS = (
     "EA_OK", "EA_ERR_ARG", "EA_ERR_ALIGN", "EA_ERR_HIP", "EA_ERR_UNSUPPORTED",
-    "EA_Q_NONE", "EA_Q_SCALED_SIGN", "EA_Q_STOCH_UNIFORM", "EA_Q_DET_UNIFORM", "EA_Q_POW2",
+    "EA_Q_NONE", "EA_Q_SCALED_SIGN", "EA_Q_STOCH_UNIFORM", "EA_Q_DET_UNIFORM", "EA_Q_POW2", "EA_Q_TOPK", "EA_Q_RANDK",
     "EA_SCALE_L1", "EA_SCALE_L2", "EA_SCALE_MAX", "EA_ADAM_AT_SERVER", "EA_ADAM_AT_WORKER",
     "EA_SCHED_CONSTANT", "EA_SCHED_ASSUMPTION2", "EA_SCHED_STEP_DECAY",
     "Quant", "Config", "Schedule", "EAError", "lib", "LIB_PATH",

@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libea.so")
 
 EA_OK, EA_ERR_ARG, EA_ERR_ALIGN, EA_ERR_HIP, EA_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
-EA_Q_NONE, EA_Q_SCALED_SIGN, EA_Q_STOCH_UNIFORM, EA_Q_DET_UNIFORM, EA_Q_POW2 = 0, 1, 2, 3, 4
+EA_Q_NONE, EA_Q_SCALED_SIGN, EA_Q_STOCH_UNIFORM, EA_Q_DET_UNIFORM, EA_Q_POW2, EA_Q_TOPK, EA_Q_RANDK = 0, 1, 2, 3, 4, 5, 6
 EA_SCALE_L1, EA_SCALE_L2, EA_SCALE_MAX = 0, 1, 2
 EA_ADAM_AT_SERVER, EA_ADAM_AT_WORKER = 0, 1
 EA_SCHED_CONSTANT, EA_SCHED_ASSUMPTION2, EA_SCHED_STEP_DECAY = 0, 1, 2
@@ -23,7 +23,8 @@ class Quant(C.Structure):
     """ea_quant_t"""
     _fields_ = [("kind", C.c_int32), ("scale", C.c_int32), ("bits", C.c_int32),
                 ("error_feedback", C.c_int32), ("bucket", C.c_int64),
-                ("pow2_kmin", C.c_int32), ("pow2_kmax", C.c_int32)]
+                ("pow2_kmin", C.c_int32), ("pow2_kmax", C.c_int32), ("keep", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class Config(C.Structure):
@@ -39,7 +40,7 @@ class Schedule(C.Structure):
                 ("T", C.c_int64), ("period", C.c_int64)]
 
 
-assert C.sizeof(Quant) == 32 and C.sizeof(Config) == 104 and C.sizeof(Schedule) == 32
+assert C.sizeof(Quant) == 40 and C.sizeof(Config) == 120 and C.sizeof(Schedule) == 32
 
 
 class EAError(RuntimeError):

@@ -34,6 +34,11 @@ bool kind_has_scales(int32_t kind)
     return kind == EA_Q_SCALED_SIGN || kind == EA_Q_STOCH_UNIFORM || kind == EA_Q_DET_UNIFORM;
 }
 
+bool kind_is_sparse(int32_t kind)
+{
+    return kind == EA_Q_TOPK || kind == EA_Q_RANDK;
+}
+
 // Code width of a quantizer (validated), or a negative error.
 int32_t bits_of(const ea_quant_t* q)
 {
@@ -54,6 +59,9 @@ int32_t bits_of(const ea_quant_t* q)
         while ((1 << b) < need) ++b;
         return 1 + b;
     }
+    case EA_Q_TOPK:
+    case EA_Q_RANDK:
+        return q->keep >= 1 ? 1 : EA_ERR_ARG;
     default:
         return EA_ERR_ARG;
     }
@@ -71,6 +79,7 @@ int64_t bucket_len(const ea_quant_t* q, int64_t d)
 
 int64_t nscales_of(const ea_quant_t* q, int64_t d)
 {
+    if (kind_is_sparse(q->kind)) return (d + q->bucket - 1) / q->bucket * q->keep;
     if (!kind_has_scales(q->kind)) return 0;
     const int64_t B = bucket_len(q, d);
     return (d + B - 1) / B;
@@ -84,8 +93,9 @@ int64_t words_of(int32_t b, int64_t d)
 int check_quant(const ea_quant_t* q, int64_t d, const char* side)
 {
     const int32_t b = bits_of(q);
-    if (b < 0) return fail(EA_ERR_ARG, "%s quantizer: invalid kind %d / bits %d / pow2 range [%d, %d]", side,
-                           q->kind, q->bits, q->pow2_kmin, q->pow2_kmax);
+    if (b < 0)
+        return fail(EA_ERR_ARG, "%s quantizer: invalid kind %d / bits %d / pow2 range [%d, %d] / keep %d", side,
+                    q->kind, q->bits, q->pow2_kmin, q->pow2_kmax, q->keep);
     if (q->kind == EA_Q_STOCH_UNIFORM && q->scale != EA_SCALE_L2 && q->scale != EA_SCALE_MAX)
         return fail(EA_ERR_ARG, "%s quantizer: stochastic uniform needs EA_SCALE_L2 or EA_SCALE_MAX", side);
     if (q->error_feedback != 0 && q->error_feedback != 1)
@@ -97,6 +107,15 @@ int check_quant(const ea_quant_t* q, int64_t d, const char* side)
             return fail(EA_ERR_UNSUPPORTED, "%s quantizer: bucket %lld must be 256, 512, 1024, 2048, 0 or >= d",
                         side, (long long)B);
     }
+    if (kind_is_sparse(q->kind)) {
+        const int64_t B = q->bucket;
+        if (B != 256 && B != 512 && B != 1024 && B != 2048)
+            return fail(EA_ERR_UNSUPPORTED, "%s quantizer: top-k / random-k bucket %lld must be 256, 512, 1024 or 2048",
+                        side, (long long)B);
+        if (q->keep > B)
+            return fail(EA_ERR_ARG, "%s quantizer: keep %d must be in [1, bucket %lld]", side, q->keep, (long long)B);
+    }
+    if (q->reserved != 0) return fail(EA_ERR_ARG, "%s quantizer: reserved field must be 0", side);
     return EA_OK;
 }
 
@@ -116,8 +135,10 @@ ea::QDev make_qdev(const ea_quant_t* q, int64_t d)
     r.ef = q->error_feedback;
     r.norm = q->kind == EA_Q_SCALED_SIGN ? ea::S_L1
            : (q->kind == EA_Q_STOCH_UNIFORM && q->scale == EA_SCALE_L2) ? ea::S_L2 : ea::S_MAX;
-    r.B = kind_has_scales(q->kind) ? bucket_len(q, d) : d;
-    r.cpb = (kind_has_scales(q->kind) && !one_bucket(q, d)) ? (int32_t)(q->bucket / 256) : 0;
+    r.B = kind_has_scales(q->kind) ? bucket_len(q, d) : kind_is_sparse(q->kind) ? q->bucket : d;
+    r.cpb = ((kind_has_scales(q->kind) && !one_bucket(q, d)) || kind_is_sparse(q->kind)) ? (int32_t)(q->bucket / 256)
+                                                                                          : 0;
+    r.keep = kind_is_sparse(q->kind) ? q->keep : 0;
     r.cpb_shift = 0;
     while (r.cpb > 0 && (1 << r.cpb_shift) < r.cpb) ++r.cpb_shift;
     r.L = q->kind == EA_Q_STOCH_UNIFORM ? (1 << r.bits) - 1 : q->kind == EA_Q_DET_UNIFORM ? (1 << (r.bits - 1)) - 1 : 0;

@@ -27,7 +27,7 @@ __device__ __forceinline__ int lane_id()
     return (int)(threadIdx.x & (kWave - 1));
 }
 
-enum : int32_t { Q_NONE = 0, Q_SCALED_SIGN = 1, Q_STOCH = 2, Q_DET = 3, Q_POW2 = 4 };
+enum : int32_t { Q_NONE = 0, Q_SCALED_SIGN = 1, Q_STOCH = 2, Q_DET = 3, Q_POW2 = 4, Q_TOPK = 5, Q_RANDK = 6 };
 enum : int32_t { S_L1 = 0, S_L2 = 1, S_MAX = 2 };
 enum : int32_t { AT_SERVER = 0, AT_WORKER = 1 };
 
@@ -42,6 +42,7 @@ struct QDev {
     int32_t L;          // STOCH: 2^b - 1; DET: 2^(b-1) - 1
     int32_t kmin;       // POW2: smallest exponent
     int32_t kmax;       // POW2: largest exponent
+    int32_t keep;       // TOPK, RANDK: elements kept per bucket
     int64_t B;          // bucket length in elements (d for one bucket)
     int64_t nscales;    // scales per message
     int64_t words;      // uint64 words per message
@@ -77,6 +78,14 @@ __device__ __forceinline__ bool has_scale(const QDev& q)
 {
     const int k = QT::kind(q);
     return k == Q_SCALED_SIGN || k == Q_STOCH || k == Q_DET;
+}
+
+// Definition 3 sparsifiers: a kept-mask code plus `keep` values per bucket.
+template <class QT>
+__device__ __forceinline__ bool is_sparse(const QDev& q)
+{
+    const int k = QT::kind(q);
+    return k == Q_TOPK || k == Q_RANDK;
 }
 
 // ---------------------------------------------------------------------------
@@ -455,6 +464,12 @@ __device__ __forceinline__ float4 sub4(float4 a, float4 b)
 __device__ __forceinline__ float4 zero4()
 {
     return make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+}
+
+// Number of set bits of a wave mask that belong to lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
 // v_writelane_b32: write a wave-uniform 32-bit value into one lane of a VGPR.

@@ -126,6 +126,156 @@ __device__ __forceinline__ WordSink message_sink(const QDev& q, uint64_t* codes,
     return sink;
 }
 
+// Definition 3 sparsifiers (TOPK, RANDK) on one tile.  Each bucket keeps
+// its k = min(keep, n) highest-ranked elements by a 32-bit key, larger keys
+// first and lower element indices first among equal keys: the magnitude's
+// bit pattern (TOPK) or the element's 24-bit draw word (RANDK).  The k-th
+// largest key is found by a bitwise search from the top bit, one ballot per
+// key slot counting the keys that reach a candidate; it stops as soon as
+// exactly k keys reach the candidate, which then splits the bucket without
+// ties.  Otherwise keys equal to the threshold are ranked by element index
+// (element n = 256c + 4l + s comes after every element of lower chunks, of
+// lower lanes of its chunk, and of lower slots of its lane).  The kept
+// values are listed in element order at positions counted the same way.
+// Elements past d get key 0 and the highest indices, so they rank below
+// every element of the vector and are never kept.
+template <int C, bool FULL, class QT>
+__device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C], int64_t base, int nch, int64_t d,
+                                              uint32_t k0, uint32_t k1, uint32_t step, uint32_t sid,
+                                              float* __restrict__ vals, WordSink& sink, float4 (&deq)[C])
+{
+    const int lane = lane_id();
+    const int cpb = QT::cpb(q);
+    const bool topk = QT::kind(q) == Q_TOPK;
+    if (FULL) nch = C;
+
+    uint32_t key[C][4];
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
+        const int nv = FULL ? 4 : (ch < nch ? nvalid4(n, d) : 0);
+        uint4 r = make_uint4(0u, 0u, 0u, 0u);
+        if (!topk && (FULL || ch < nch)) {
+            const uint64_t j = (uint64_t)n >> 2;
+            r = philox10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), step, sid), k0, k1);
+        }
+        const uint32_t rr[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t kv = topk ? (__float_as_uint(comp(p[ch], k)) & 0x7FFFFFFFu) : (rr[k] >> 8);
+            key[ch][k] = (FULL || k < nv) ? kv : 0u;
+        }
+        deq[ch] = zero4();
+    }
+
+    const int64_t chunk0 = base >> 8;
+#pragma unroll
+    for (int b0 = 0; b0 < C; ++b0) {
+        if ((b0 & (cpb - 1)) != 0) continue;
+        if (!FULL && b0 >= nch) continue;
+        const int64_t e0 = base + (int64_t)b0 * kChunk;
+        const int64_t nb = FULL ? q.B : ((d - e0) < q.B ? (d - e0) : q.B);
+        const uint32_t kk = (uint32_t)(nb < q.keep ? nb : q.keep);
+
+        // Threshold: the largest T with at least kk keys >= T.
+        uint32_t T = 0u;
+        bool exact = false;
+        for (int bit = topk ? 30 : 23; bit >= 0; --bit) {
+            const uint32_t cand = T | (1u << bit);
+            uint32_t cnt = 0;
+#pragma unroll
+            for (int j = 0; j < C; ++j) {
+                if (j < b0 || j >= b0 + cpb) continue;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    cnt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key[j][k] >= cand));
+            }
+            if (cnt >= kk) {
+                T = cand;
+                if (cnt == kk) {
+                    exact = true;
+                    break;
+                }
+            }
+        }
+
+        // Kept flags, bit 4j + k of a lane for its element in chunk j, slot k.
+        uint32_t kbits = 0u;
+        if (exact) {
+#pragma unroll
+            for (int j = 0; j < C; ++j) {
+                if (j < b0 || j >= b0 + cpb) continue;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) kbits |= (key[j][k] >= T ? 1u : 0u) << (4 * j + k);
+            }
+        } else {
+            uint32_t gt = 0;
+#pragma unroll
+            for (int j = 0; j < C; ++j) {
+                if (j < b0 || j >= b0 + cpb) continue;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    gt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key[j][k] > T));
+            }
+            const uint32_t need = kk - gt;
+            uint32_t before = 0;
+#pragma unroll
+            for (int j = 0; j < C; ++j) {
+                if (j < b0 || j >= b0 + cpb) continue;
+                uint32_t below = 0, tot = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint64_t em = __builtin_amdgcn_ballot_w64(key[j][k] == T);
+                    below += lanes_below(em);
+                    tot += (uint32_t)__builtin_popcountll(em);
+                }
+                uint32_t own = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const bool eq = key[j][k] == T;
+                    const bool kept = key[j][k] > T || (eq && before + below + own < need);
+                    kbits |= (kept ? 1u : 0u) << (4 * j + k);
+                    own += eq ? 1u : 0u;
+                }
+                before += tot;
+            }
+        }
+
+        // Code words, values in element order, and the dequantized tile.  A
+        // plain store: the caches merge the bucket's scattered 4-byte values.
+        float* vb = vals + ((chunk0 + b0) >> QT::cpb_shift(q)) * (int64_t)q.keep;
+        uint32_t before = 0;
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            if (j < b0 || j >= b0 + cpb) continue;
+            if (!FULL && j >= nch) continue;
+            uint64_t km[4];
+            uint32_t below = 0, tot = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                km[k] = __builtin_amdgcn_ballot_w64(((kbits >> (4 * j + k)) & 1u) != 0u);
+                below += lanes_below(km[k]);
+                tot += (uint32_t)__builtin_popcountll(km[k]);
+            }
+            uint32_t own = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const bool kept = ((kbits >> (4 * j + k)) & 1u) != 0u;
+                const float x = comp(p[j], k);
+                const uint32_t pos = before + below + own;   // < kk by construction; guarded all the same
+                if (kept && pos < (uint32_t)q.keep) vb[pos] = x;
+                own += kept ? 1u : 0u;
+                set_comp(deq[j], k, kept ? x : 0.0f);
+                sink.put(km[k]);
+            }
+            before += tot;
+        }
+        // A bucket shorter than keep: the remaining value slots are zero.
+        if (!FULL)
+            for (uint32_t sl = kk + (uint32_t)lane; sl < (uint32_t)q.keep; sl += kWave) vb[sl] = 0.0f;
+    }
+}
+
 template <int C, bool FULL, class QT>
 __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, const float4 (&p)[C],
                                               int64_t base, int nch, int64_t d, uint32_t k0, uint32_t k1,
@@ -133,6 +283,10 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
                                               uint64_t* __restrict__ codes, float* __restrict__ scales,
                                               WordSink& sink, float4 (&deq)[C])
 {
+    if (is_sparse<QT>(q)) {
+        sparsify_tile<C, FULL, QT>(q, p, base, nch, d, k0, k1, step, sid, scales, sink, deq);
+        return;
+    }
     const int lane = lane_id();
     const int kind = QT::kind(q);
     const int norm = QT::norm(q);
@@ -271,6 +425,40 @@ __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, co
 {
     const int lane = lane_id();
     const int bits = QT::bits(q);
+    if (is_sparse<QT>(q)) {
+        // Kept elements take their bucket's values in element order; the
+        // count of kept elements before a chunk restarts at each bucket.
+        uint32_t before = 0;
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) {
+            deq[ch] = zero4();
+            if (ch >= nch) continue;
+            const int64_t chunk = (base >> 8) + ch;
+            if ((chunk & (QT::cpb(q) - 1)) == 0) before = 0;
+            const uint64_t* w = codes + chunk * 4;
+            const float* vb = scales + (chunk >> QT::cpb_shift(q)) * (int64_t)q.keep;
+            uint64_t m[4];
+            uint32_t below = 0, tot = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                m[k] = w[k];
+                below += lanes_below(m[k]);
+                tot += (uint32_t)__builtin_popcountll(m[k]);
+            }
+            uint32_t own = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                // A mask with more than keep bits in a bucket (not a message
+                // this library wrote) reads no value past the bucket's slots.
+                const bool kept = ((m[k] >> lane) & 1u) != 0u;
+                const uint32_t pos = before + below + own;
+                set_comp(deq[ch], k, kept && pos < (uint32_t)q.keep ? vb[pos] : 0.0f);
+                own += kept ? 1u : 0u;
+            }
+            before += tot;
+        }
+        return;
+    }
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
@@ -924,6 +1112,8 @@ using SignQ2 = QCt<Q_SCALED_SIGN, 1, S_L1, 2>;
 using Stoch4L2Q2 = QCt<Q_STOCH, 4, S_L2, 2>;
 using Stoch2MaxQ2 = QCt<Q_STOCH, 2, S_MAX, 2>;
 using Stoch2MaxQ4 = QCt<Q_STOCH, 2, S_MAX, 4>;
+using TopKQ2 = QCt<Q_TOPK, 1, S_MAX, 2>;
+using RandKQ2 = QCt<Q_RANDK, 1, S_MAX, 2>;
 
 struct Special {
     int C;
@@ -951,6 +1141,8 @@ const Special kSpecials[] = {
     EA_SPECIAL(4, Stoch2MaxQ4, SignQ4, AT_SERVER),
     EA_SPECIAL(4, Stoch2MaxQ4, SignQ4, AT_WORKER),
     EA_SPECIAL(2, SignQ2, SignQ2, AT_SERVER),
+    EA_SPECIAL(2, TopKQ2, TopKQ2, AT_SERVER),
+    EA_SPECIAL(2, RandKQ2, RandKQ2, AT_SERVER),
 };
 
 const Special* find_special(const StepArgs& a, int C)

@@ -6,6 +6,8 @@ Comparison rule
     two sides; such a scale can differ by at most one binary32 ulp (its
     binary64 sum is formed in a different order) and the code flips it causes
     are counted as rounding-boundary ties (at most 1e-6 of the entries).
+  * top-k / random-k messages: kept masks and kept values bit-exact (the
+    selection is an integer decision on keys both sides compute exactly).
   * scales, e_w, e_s, x, m, v: |gpu - oracle| <= 1e-5 * |oracle| + floor, the
     floor being 1e-8 of the largest magnitude of that array.
 After a step with any tie the GPU state is reset to the oracle's (counted).
@@ -22,9 +24,20 @@ from paper_2205_14473_amd.state import allocate, init_state
 REL_TOL = 1e-5
 
 
-def qfields(kind, bits=0, scale=O.SCALE_L2, ef=1, bucket=0, kmin=0, kmax=0):
+def qfields(kind, bits=0, scale=O.SCALE_L2, ef=1, bucket=0, kmin=0, kmax=0, keep=0):
     return dict(kind=kind, scale=scale, bits=bits, error_feedback=ef, bucket=bucket, pow2_kmin=kmin,
-                pow2_kmax=kmax)
+                pow2_kmax=kmax, keep=keep)
+
+
+SPARSE_KINDS = (O.Q_TOPK, O.Q_RANDK)
+
+
+def same_values(got, want):
+    """Bit-identical binary32 arrays (any NaN matches any NaN)."""
+    got = np.ascontiguousarray(got, np.float32)
+    want = np.ascontiguousarray(want, np.float32)
+    same = got.view(np.uint32) == want.view(np.uint32)
+    return bool(np.all(same | (np.isnan(got) & np.isnan(want))))
 
 
 def configs(d, N, qw, qs, placement=O.ADAM_AT_SERVER, seed=1, beta1=0.9, beta2=0.999, lr=1e-3, eps=1e-8):
@@ -119,6 +132,7 @@ class Pair:
         self.stats = Stats()
         self.bw, self.bs = O.code_bits(self.oc.qw), O.code_bits(self.oc.qs)
         self.nsw, self.nss = E.ea_msg_scales(self.ec.qw, d), E.ea_msg_scales(self.ec.qs, d)
+        self.sparse_w, self.sparse_s = self.oc.qw.kind in SPARSE_KINDS, self.oc.qs.kind in SPARSE_KINDS
         torch.cuda.synchronize()
 
     def oracle_config(self, t):
@@ -177,19 +191,25 @@ class Pair:
         ties = 0
         ws_g = rb.wscales.cpu().numpy()[:, :self.nsw]
         ss_g = rb.sscales.cpu().numpy()[:self.nss]
-        if self.nsw:
+        if self.sparse_w:
+            assert same_values(ws_g, out["wscales"]), "worker kept values differ"
+        elif self.nsw:
             assert np.all(_ulp_diff(ws_g, out["wscales"]) <= 1), "worker scales differ by more than 1 ulp"
             s.scale_ties += int((ws_g != out["wscales"]).sum())
-        if self.nss:
+        if self.sparse_s:
+            assert same_values(ss_g, out["sscales"]), "server kept values differ"
+        elif self.nss:
             assert np.all(_ulp_diff(ss_g, out["sscales"]) <= 1), "server scales differ by more than 1 ulp"
             s.scale_ties += int((ss_g != out["sscales"]).sum())
+        wsc = self.nsw and not self.sparse_w
+        ssc = self.nss and not self.sparse_s
         wc = rb.wcodes.cpu().numpy()
         for i in range(self.N):
             ties += _codes_match(self.oc.qw, self.bw, self.d, 0, wc[i], out["wcodes"][i],
-                                 ws_g[i] if self.nsw else None, out["wscales"][i] if self.nsw else None,
+                                 ws_g[i] if wsc else None, out["wscales"][i] if wsc else None,
                                  s, f"worker {i} codes")
         ties += _codes_match(self.oc.qs, self.bs, self.d, 0, rb.scodes.cpu().numpy(), out["scodes"],
-                             ss_g if self.nss else None, out["sscales"] if self.nss else None, s, "server codes")
+                             ss_g if ssc else None, out["sscales"] if ssc else None, s, "server codes")
         s.code_entries += (self.N + 1) * self.d
         s.code_ties += ties
         close("wscales", ws_g, out["wscales"], s)

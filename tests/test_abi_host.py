@@ -45,6 +45,10 @@ QUANTS = [
     dict(kind=3, bits=7, bucket=256),
     dict(kind=4, pow2_kmin=-17, pow2_kmax=-11),
     dict(kind=4, pow2_kmin=-126, pow2_kmax=127),
+    dict(kind=5, bucket=512, keep=16),
+    dict(kind=5, bucket=256, keep=1),
+    dict(kind=6, bucket=2048, keep=2048),
+    dict(kind=6, bucket=1024, keep=77),
 ]
 
 
@@ -77,7 +81,10 @@ def test_invalid_config_rejected(E, field, value, code):
     (dict(kind=9), -1), (dict(kind=2, scale=1, bits=3, bucket=512), -1), (dict(kind=2, scale=0, bits=2), -1),
     (dict(kind=3, bits=1), -1), (dict(kind=4, pow2_kmin=-3, pow2_kmax=-3), -1),
     (dict(kind=1, bucket=768), -4), (dict(kind=1, bucket=4096), -4), (dict(kind=1, bucket=-5), -1),
-    (dict(kind=1, error_feedback=2, bucket=512), -1)])
+    (dict(kind=1, error_feedback=2, bucket=512), -1),
+    (dict(kind=5, bucket=512, keep=0), -1), (dict(kind=6, bucket=512, keep=513), -1),
+    (dict(kind=5, bucket=0, keep=4), -4), (dict(kind=6, bucket=768, keep=4), -4),
+    (dict(kind=5, bucket=4096, keep=4), -4), (dict(kind=5, bucket=512, keep=4, reserved=1), -1)])
 def test_invalid_quantizer_rejected(E, qd, code):
     assert E.ea_validate(_cfg(E, qw=E.Quant(**qd))) == code
     assert E.ea_validate(_cfg(E, qs=E.Quant(**qd))) == code

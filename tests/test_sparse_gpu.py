@@ -1,0 +1,101 @@
+"""GPU parity of the Definition 3 sparsifiers (top-k and random-k per bucket)
+against the oracle: kept masks and kept values bit-exact, state within the
+float tolerance, after every step of a trajectory.  Covers the specialized
+whole-tile kernels (bucket 512, Adam at the server), the generic kernels, the
+split calls (which decode the messages), ragged and tiny sizes, equal keys at
+the threshold, and keep at its limits."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU-only host
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from parity_util import Pair, qfields  # noqa: E402
+
+TOPK = lambda keep, b, ef=1: qfields(O.Q_TOPK, bucket=b, keep=keep, ef=ef)  # noqa: E731
+RANDK = lambda keep, b, ef=1: qfields(O.Q_RANDK, bucket=b, keep=keep, ef=ef)  # noqa: E731
+SPARSE = {"topk": TOPK, "randk": RANDK}
+
+
+def _grads(gen, seed, t, N, d):
+    w = W.Workload("t", "t", d, N, None, None, 1, seed, gen)
+    return W.host_gradients(w, t, d=d)
+
+
+def _tied_grads(seed, t, N, d):
+    """Few distinct magnitudes and many zeros: most keys tie."""
+    rng = np.random.default_rng(seed * 1000 + t)
+    mag = rng.choice(np.array([0.0, 0.0, 1e-3, 2e-3, 4e-3], np.float32), size=(N, d))
+    return (mag * rng.choice(np.array([-1.0, 1.0], np.float32), size=(N, d))).astype(np.float32)
+
+
+def _run(d, N, qw, qs, placement, T, gen="student_t", seed=5, split=False, **hp):
+    pair = Pair(d, N, qw, qs, placement, seed=seed, split=split, **hp)
+    for t in range(1, T + 1):
+        g = _tied_grads(seed, t, N, d) if gen == "tied" else _grads(gen, seed, t, N, d)
+        pair.step(t, g)
+    pair.check_tie_budget()
+    print(f"\n[parity] sparse d={d} N={N} T={T} placement={placement} split={split}: {pair.stats}", flush=True)
+    return pair
+
+
+@pytest.mark.parametrize("kind", list(SPARSE))
+@pytest.mark.parametrize("d", [512 * 41 + 384, 512 * 42, 512 * 41, 512 + 100, 300])
+def test_lean_kernels(kind, d):
+    """Bucket 512, Adam at the server, 16 workers: the specialized two-tile
+    kernels plus the edge kernel of a ragged tail."""
+    q = SPARSE[kind](16, 512)
+    _run(d, 16, q, q, O.ADAM_AT_SERVER, T=4)
+
+
+@pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
+@pytest.mark.parametrize("kind", list(SPARSE))
+@pytest.mark.parametrize("bucket,keep", [(256, 1), (512, 37), (1024, 200), (2048, 64)])
+def test_generic_kernels(kind, bucket, keep, placement):
+    q = SPARSE[kind](keep, bucket)
+    _run(4 * 1024 + 260, 3, q, q, placement, T=4, gen="outliers")
+
+
+@pytest.mark.parametrize("kind", list(SPARSE))
+def test_split_calls(kind):
+    q = SPARSE[kind](24, 512)
+    _run(512 * 9 + 130, 5, q, q, O.ADAM_AT_SERVER, T=4, split=True)
+    _run(256 * 7 + 3, 3, SPARSE[kind](5, 256), TOPK(100, 1024), O.ADAM_AT_WORKER, T=3, split=True)
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["fused", "split"])
+def test_equal_keys_at_the_threshold(split):
+    _run(512 * 9 + 200, 16, TOPK(16, 512), TOPK(16, 512), O.ADAM_AT_SERVER, T=4, gen="tied", split=split)
+    _run(256 * 11 + 17, 3, TOPK(40, 256), TOPK(9, 512), O.ADAM_AT_WORKER, T=4, gen="tied", split=split)
+
+
+@pytest.mark.parametrize("d", [1, 3, 100, 255, 256, 257, 1001])
+def test_tiny_and_unaligned_sizes(d):
+    """Sizes below a bucket and rows without 16-byte alignment; a bucket
+    shorter than keep zero-fills its remaining value slots."""
+    _run(d, 3, TOPK(4, 256), RANDK(300, 512), O.ADAM_AT_SERVER, T=3)
+    _run(d, 2, RANDK(1, 256), TOPK(256, 256), O.ADAM_AT_WORKER, T=3)
+
+
+@pytest.mark.parametrize("kind", list(SPARSE))
+def test_keep_limits(kind):
+    """keep = bucket sends everything (Q is the identity), keep = 1 one element."""
+    _run(512 * 5 + 64, 4, SPARSE[kind](512, 512), SPARSE[kind](1, 512), O.ADAM_AT_SERVER, T=3)
+
+
+def test_mixed_with_quantizers():
+    """A sparsifier on one side, a scaled quantizer on the other."""
+    _run(2048 * 3 + 500, 4, TOPK(64, 2048), qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 1, 256), O.ADAM_AT_SERVER,
+         T=3)
+    _run(1024 * 5 + 12, 3, qfields(O.Q_STOCH_UNIFORM, 4, O.SCALE_L2, 1, 512), RANDK(32, 1024), O.ADAM_AT_WORKER,
+         T=3)
+
+
+def test_error_feedback_off():
+    _run(512 * 6 + 10, 4, TOPK(8, 512, ef=0), RANDK(8, 512, ef=0), O.ADAM_AT_SERVER, T=3)
