@@ -126,14 +126,86 @@ __device__ __forceinline__ WordSink message_sink(const QDev& q, uint64_t* codes,
     return sink;
 }
 
+// Sparsifier tuning: how many of each lane's largest keys a first threshold
+// search runs on (0: none, 1 to 3), and whether the searches skip the bits
+// that all lane maxima share (1).
+#ifndef EA_SPARSE_SUBSET
+#define EA_SPARSE_SUBSET 3
+#endif
+#ifndef EA_SPARSE_PREFIX
+#define EA_SPARSE_PREFIX 1
+#endif
+
+// Threshold search over values the wave counts with count(c) = how many are
+// >= c (non-increasing in c): the largest T with count(T) >= kk, built bit by
+// bit from `top` down above a prefix T0 whose bits from `top` down are zero
+// and which the answer is known to share; or, as soon as some accepted
+// candidate is reached by exactly kk values, that candidate with exact set.
+// Each step is one ballot per counted value slot; the loop is kept rolled
+// (unrolling it measured no faster and multiplies the code).
+template <class Count>
+__device__ __forceinline__ uint32_t bit_select(const Count& count, uint32_t kk, int top, uint32_t T0, bool& exact)
+{
+    uint32_t T = T0;
+    exact = false;
+#pragma nounroll
+    for (int bit = top; bit >= 0; --bit) {
+        const uint32_t cand = T | (1u << bit);
+        const uint32_t n = count(cand);
+        if (n >= kk) {
+            T = cand;
+            if (n == kk) {
+                exact = true;
+                break;
+            }
+        }
+    }
+    return T;
+}
+
+__device__ __forceinline__ uint32_t wave_count(bool pred)
+{
+    return (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(pred));
+}
+
+// Bitwise OR and AND of a value over the wave (same steps as wave_max).
+__device__ __forceinline__ void wave_or_and(uint32_t v, uint32_t& o, uint32_t& a)
+{
+    o = v;
+    a = v;
+    o |= dpp<kDppXor1>(o);
+    a &= dpp<kDppXor1>(a);
+    o |= dpp<kDppXor2>(o);
+    a &= dpp<kDppXor2>(a);
+    o |= dpp<kDppHalfMirror>(o);
+    a &= dpp<kDppHalfMirror>(a);
+    o |= dpp<kDppRowMirror>(o);
+    a &= dpp<kDppRowMirror>(a);
+    uint32_t x, y;
+    row_swap16(o, x, y);
+    o = x | y;
+    row_swap16(a, x, y);
+    a = x & y;
+    row_swap32(o, x, y);
+    o = x | y;
+    row_swap32(a, x, y);
+    a = x & y;
+}
+
 // Definition 3 sparsifiers (TOPK, RANDK) on one tile.  Each bucket keeps
 // its k = min(keep, n) highest-ranked elements by a 32-bit key, larger keys
 // first and lower element indices first among equal keys: the magnitude's
-// bit pattern (TOPK) or the element's 24-bit draw word (RANDK).  The k-th
-// largest key is found by a bitwise search from the top bit, one ballot per
-// key slot counting the keys that reach a candidate; it stops as soon as
-// exactly k keys reach the candidate, which then splits the bucket without
-// ties.  Otherwise keys equal to the threshold are ranked by element index
+// bit pattern (TOPK) or the element's 24-bit draw word (RANDK).
+//
+// The k-th largest key T is found by a bitwise search (bit_select) that
+// counts with ballots; the search is the costly part, so three things cut its
+// steps and ballots.  (1) For k <= 64, T lies between the smallest and the
+// largest lane maximum, so the search starts below the bits all lane maxima
+// share (for magnitudes, typically the sign and most of the exponent).  (2) It first runs on each lane's three largest keys only (3
+// ballots a step instead of 4 per chunk) and keeps that answer when a full
+// count confirms it; else it runs again over every key.  (3) It stops as
+// soon as exactly k keys reach a candidate, which then splits the bucket
+// without ties.  Otherwise the keys equal to T are ranked by element index
 // (element n = 256c + 4l + s comes after every element of lower chunks, of
 // lower lanes of its chunk, and of lower slots of its lane).  The kept
 // values are listed in element order at positions counted the same way.
@@ -147,6 +219,7 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
     const int lane = lane_id();
     const int cpb = QT::cpb(q);
     const bool topk = QT::kind(q) == Q_TOPK;
+    const int top = topk ? 31 : 23;   // keys below 2^31 (TOPK) or 2^24 (RANDK)
     if (FULL) nch = C;
 
     uint32_t key[C][4];
@@ -177,27 +250,71 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
         const int64_t nb = FULL ? q.B : ((d - e0) < q.B ? (d - e0) : q.B);
         const uint32_t kk = (uint32_t)(nb < q.keep ? nb : q.keep);
 
-        // Threshold: the largest T with at least kk keys >= T.
-        uint32_t T = 0u;
-        bool exact = false;
-        for (int bit = topk ? 30 : 23; bit >= 0; --bit) {
-            const uint32_t cand = T | (1u << bit);
-            uint32_t cnt = 0;
+        // Threshold T: the kk-th largest key of the bucket.
+        const auto count_all = [&](uint32_t c) {
+            uint32_t n = 0u;
 #pragma unroll
             for (int j = 0; j < C; ++j) {
                 if (j < b0 || j >= b0 + cpb) continue;
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    cnt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key[j][k] >= cand));
+                for (int k = 0; k < 4; ++k) n += wave_count(key[j][k] >= c);
             }
-            if (cnt >= kk) {
-                T = cand;
-                if (cnt == kk) {
-                    exact = true;
-                    break;
-                }
+            return n;
+        };
+        uint32_t T = 0u, gt = 0u;
+        bool exact = false, found = false, have_gt = false;
+        // The lanes' largest keys m[0] (and next largest m[1], m[2]).
+        uint32_t m[3] = {0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            if (j < b0 || j >= b0 + cpb) continue;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t x = key[j][k];
+                if (EA_SPARSE_SUBSET > 2) m[2] = max(m[2], min(m[1], x));
+                if (EA_SPARSE_SUBSET > 1) m[1] = max(m[1], min(m[0], x));
+                m[0] = max(m[0], x);
             }
         }
+        // With kk <= 64 the threshold lies between the smallest and largest
+        // lane maximum (64 keys reach the smallest), so it has the bits that
+        // every lane maximum shares above the highest bit where they differ.
+        int hi = top;
+        uint32_t prefix = 0u;
+        if (EA_SPARSE_PREFIX && kk <= (uint32_t)kWave) {
+            uint32_t o, n;
+            wave_or_and(m[0], o, n);
+            o = (uint32_t)__builtin_amdgcn_readfirstlane((int)o);
+            n = (uint32_t)__builtin_amdgcn_readfirstlane((int)n);
+            // bits above h: all of them for h < 0, none for h >= 31
+            const auto above = [](int h) { return h < 0 ? 0xFFFFFFFFu : (h >= 31 ? 0u : ~((2u << h) - 1u)); };
+            hi = o == n ? -1 : 31 - __builtin_clz(o ^ n);
+            if (hi > top) hi = top;
+            prefix = n & above(hi);
+        }
+        if (EA_SPARSE_SUBSET > 0 && kk <= (uint32_t)(EA_SPARSE_SUBSET * kWave)) {
+            // First on the keys that are among their lane's EA_SPARSE_SUBSET
+            // largest.  Its answer Tr holds for the bucket when the counts
+            // agree: every key above Tr is among them (Tr is then the kk-th
+            // largest of all), or, when exactly kk of them reach Tr, exactly
+            // kk keys of the bucket do.
+            const auto count_sub = [&](uint32_t c) {
+                uint32_t n = 0u;
+#pragma unroll
+                for (int r = 0; r < EA_SPARSE_SUBSET; ++r) n += wave_count(m[r] >= c);
+                return n;
+            };
+            bool er;
+            const uint32_t Tr = bit_select(count_sub, kk, hi, prefix, er);
+            if (er) {
+                found = exact = count_all(Tr) == kk;
+            } else {
+                gt = count_all(Tr + 1u);
+                found = have_gt = gt == count_sub(Tr + 1u);
+            }
+            T = Tr;
+        }
+        if (!found) T = bit_select(count_all, kk, hi, prefix, exact);
 
         // Kept flags, bit 4j + k of a lane for its element in chunk j, slot k.
         uint32_t kbits = 0u;
@@ -209,13 +326,15 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
                 for (int k = 0; k < 4; ++k) kbits |= (key[j][k] >= T ? 1u : 0u) << (4 * j + k);
             }
         } else {
-            uint32_t gt = 0;
+            if (!have_gt) {
+                gt = 0u;
 #pragma unroll
-            for (int j = 0; j < C; ++j) {
-                if (j < b0 || j >= b0 + cpb) continue;
+                for (int j = 0; j < C; ++j) {
+                    if (j < b0 || j >= b0 + cpb) continue;
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    gt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key[j][k] > T));
+                    for (int k = 0; k < 4; ++k)
+                        gt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key[j][k] > T));
+                }
             }
             const uint32_t need = kk - gt;
             uint32_t before = 0;

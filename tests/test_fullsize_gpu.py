@@ -18,7 +18,7 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 import paper_2205_14473_amd as E  # noqa: E402
 from paper_2205_14473_amd.state import allocate, init_state  # noqa: E402
-from parity_util import Stats, _codes_match, _ulp_diff, close, configs  # noqa: E402
+from parity_util import SPARSE_KINDS, Stats, _codes_match, _ulp_diff, close, configs, same_values  # noqa: E402
 
 
 def _segments(d, tile, count, seed):
@@ -28,7 +28,7 @@ def _segments(d, tile, count, seed):
     return [(k * tile, min(tile, d - k * tile)) for k in sorted(picks)]
 
 
-@pytest.mark.parametrize("key", ["bert", "resnet18", "resnet50", "gpt2m"])
+@pytest.mark.parametrize("key", ["bert", "resnet18", "resnet50", "gpt2m", "bert_topk", "bert_randk"])
 def test_full_size_sampled(key):
     w = W.WORKLOADS[key]
     print(f"\n[fullsize] {w.name}", flush=True)
@@ -44,6 +44,9 @@ def test_full_size_sampled(key):
     segs = _segments(d, tile, 24, w.seed)
     bw, bs = O.code_bits(oc.qw), O.code_bits(oc.qs)
     Bw, Bs = O.bucket_len(oc.qw, d), O.bucket_len(oc.qs, d)
+    # per bucket: one scale, or keep values for a sparsifier (compared bit-exactly)
+    sp_w, sp_s = oc.qw.kind in SPARSE_KINDS, oc.qs.kind in SPARSE_KINDS
+    per_w, per_s = (oc.qw.keep if sp_w else 1), (oc.qs.keep if sp_s else 1)
     x_host = rb.x.cpu().numpy()
     states = {n0: O.State.init(oc, ln, x_host[n0:n0 + ln]) for n0, ln in segs}
     stats = Stats()
@@ -58,15 +61,17 @@ def test_full_size_sampled(key):
             out = O.step(oc, t, np.ascontiguousarray(g_host[n0]), st, n0=n0)
             w0, w1 = n0 // 256 * 4 * bw, n0 // 256 * 4 * bw + out["wcodes"].shape[1]
             v0, v1 = n0 // 256 * 4 * bs, n0 // 256 * 4 * bs + out["scodes"].shape[0]
-            ws_g = ws[:, n0 // Bw:n0 // Bw + out["wscales"].shape[1]].numpy()
-            ss_g = ss[n0 // Bs:n0 // Bs + out["sscales"].shape[0]].numpy()
-            assert np.all(_ulp_diff(ws_g, out["wscales"]) <= 1) and np.all(_ulp_diff(ss_g, out["sscales"]) <= 1)
+            ws_g = ws[:, n0 // Bw * per_w:n0 // Bw * per_w + out["wscales"].shape[1]].numpy()
+            ss_g = ss[n0 // Bs * per_s:n0 // Bs * per_s + out["sscales"].shape[0]].numpy()
+            assert same_values(ws_g, out["wscales"]) if sp_w else np.all(_ulp_diff(ws_g, out["wscales"]) <= 1)
+            assert same_values(ss_g, out["sscales"]) if sp_s else np.all(_ulp_diff(ss_g, out["sscales"]) <= 1)
             ties = 0
             for i in range(N):
-                ties += _codes_match(oc.qw, bw, d, n0, wc[i, w0:w1].numpy(), out["wcodes"][i], ws_g[i],
-                                     out["wscales"][i], stats, f"worker {i} segment {n0}")
-            ties += _codes_match(oc.qs, bs, d, n0, sc[v0:v1].numpy(), out["scodes"], ss_g, out["sscales"], stats,
-                                 f"server segment {n0}")
+                ties += _codes_match(oc.qw, bw, d, n0, wc[i, w0:w1].numpy(), out["wcodes"][i],
+                                     None if sp_w else ws_g[i], None if sp_w else out["wscales"][i], stats,
+                                     f"worker {i} segment {n0}")
+            ties += _codes_match(oc.qs, bs, d, n0, sc[v0:v1].numpy(), out["scodes"], None if sp_s else ss_g,
+                                 None if sp_s else out["sscales"], stats, f"server segment {n0}")
             stats.code_ties += ties
             stats.code_entries += (N + 1) * ln
             close("e_w", rb.e_w[:, n0:n0 + ln].cpu().numpy(), st.e_w, stats)

@@ -75,6 +75,21 @@ def test_equal_keys_at_the_threshold(split):
     _run(256 * 11 + 17, 3, TOPK(40, 256), TOPK(9, 512), O.ADAM_AT_WORKER, T=4, gen="tied", split=split)
 
 
+def test_all_keys_equal():
+    """Every key of a bucket equal (constant magnitudes; then half of them
+    zero): the lane maxima all agree, the threshold is that key, and the kept
+    elements are the lowest-indexed ones."""
+    d, N = 512 * 6 + 300, 16
+    pair = Pair(d, N, TOPK(16, 512), TOPK(16, 512), O.ADAM_AT_SERVER, seed=3)
+    rng = np.random.default_rng(12)
+    for t in range(1, 4):
+        g = (np.float32(1e-3) * rng.choice(np.array([-1.0, 1.0], np.float32), size=(N, d))).astype(np.float32)
+        if t == 2:
+            g[:, ::2] = 0.0
+        pair.step(t, g)
+    pair.check_tie_budget()
+
+
 @pytest.mark.parametrize("d", [1, 3, 100, 255, 256, 257, 1001])
 def test_tiny_and_unaligned_sizes(d):
     """Sizes below a bucket and rows without 16-byte alignment; a bucket

@@ -22,7 +22,7 @@ from typing import Dict
 
 import numpy as np
 
-Q_NONE, Q_SCALED_SIGN, Q_STOCH_UNIFORM, Q_DET_UNIFORM, Q_POW2 = 0, 1, 2, 3, 4
+Q_NONE, Q_SCALED_SIGN, Q_STOCH_UNIFORM, Q_DET_UNIFORM, Q_POW2, Q_TOPK, Q_RANDK = 0, 1, 2, 3, 4, 5, 6
 SCALE_L1, SCALE_L2, SCALE_MAX = 0, 1, 2
 ADAM_AT_SERVER, ADAM_AT_WORKER = 0, 1
 
@@ -36,11 +36,12 @@ class QSpec:
     bucket: int = 0
     pow2_kmin: int = 0
     pow2_kmax: int = 0
+    keep: int = 0
 
     def fields(self) -> Dict[str, int]:
         return dict(kind=self.kind, scale=self.scale, bits=self.bits,
                     error_feedback=self.error_feedback, bucket=self.bucket,
-                    pow2_kmin=self.pow2_kmin, pow2_kmax=self.pow2_kmax)
+                    pow2_kmin=self.pow2_kmin, pow2_kmax=self.pow2_kmax, keep=self.keep)
 
 
 @dataclass(frozen=True)
@@ -68,6 +69,7 @@ class Workload:
 
 
 SIGN1 = lambda b: QSpec(Q_SCALED_SIGN, 1, SCALE_L1, 1, b)  # noqa: E731
+SPARSE = lambda kind, keep, b: QSpec(kind, 0, SCALE_L2, 1, b, keep=keep)  # noqa: E731
 
 WORKLOADS = {
     "toy": Workload("toy", "toy-convex d=65536 N=4", 65536, 4, SIGN1(0), SIGN1(0), 100, 1, "toy"),
@@ -81,6 +83,12 @@ WORKLOADS = {
                      QSpec(Q_STOCH_UNIFORM, 4, SCALE_L2, 1, 512), 20, 4, "student_t"),
     "gpt2m": Workload("gpt2m", "GPT-2-medium-sized d=355000000 N=8", 355_000_000, 8,
                       QSpec(Q_STOCH_UNIFORM, 2, SCALE_MAX, 1, 1024), SIGN1(1024), 10, 5, "outliers"),
+    # Definition 3 compressors on the BERT-sized round: 16 of every 512 kept
+    # (a 1-bit kept mask plus 16 values per bucket: 2 bits per parameter).
+    "bert_topk": Workload("bert_topk", "BERT-base-sized d=110000000 N=16, top-16 of 512", 110_000_000, 16,
+                          SPARSE(Q_TOPK, 16, 512), SPARSE(Q_TOPK, 16, 512), 20, 4, "student_t"),
+    "bert_randk": Workload("bert_randk", "BERT-base-sized d=110000000 N=16, random-16 of 512", 110_000_000, 16,
+                           SPARSE(Q_RANDK, 16, 512), SPARSE(Q_RANDK, 16, 512), 20, 4, "student_t"),
 }
 
 # The paper's toy problem (Section V-A): 500x500, 10 workers, beta 0.9, theta 0.99.
