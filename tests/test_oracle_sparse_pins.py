@@ -139,15 +139,24 @@ def test_randk_residual_in_expectation_and_independent_of_x():
     y = rng.standard_normal(n).astype(np.float32)
     q = sq(O.Q_RANDK, keep, n)
     r2 = []
+    hits = np.zeros(n)
     for t in range(1, T + 1):
         u = O.uniforms(11, t, 4, 0, n)
         cx, dx, _ = O.quantize(q, x, u=u)
         cy, _, _ = O.quantize(q, y, u=u)
         assert np.array_equal(cx, cy)            # the kept set depends on the draws only
+        assert u[cx == 1].min() >= u[cx == 0].max()   # and holds the largest draws
         r2.append(float(np.sum((x.astype(np.float64) - dx) ** 2)))
+        hits += cx
     x2 = float(np.sum(x.astype(np.float64) ** 2))
     # E ||x - Q(x)||^2 = (1 - k/n) ||x||^2 for a uniform k-subset
     assert abs(np.mean(r2) / x2 - (1 - keep / n)) < 0.01
+    # every position is kept with probability k/n: no drift along the bucket
+    # (each half of the bucket holds half of the T*k kept elements, within 5 sigma)
+    half = hits[: n // 2].sum()
+    assert abs(half - T * keep / 2) < 5 * np.sqrt(T * keep / 4)
+    quarters = hits.reshape(4, -1).sum(1)
+    assert np.all(np.abs(quarters - T * keep / 4) < 5 * np.sqrt(T * keep * 3 / 16))
 
 
 def test_sparse_segment_equals_slice_of_full_run():
