@@ -13,13 +13,15 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libea.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("ea_kernels.hip", "ea_toy.hip", "ea_api.cpp")]
-HEADERS = [os.path.join(CSRC, f) for f in ("ea_device.hpp", "ea_launch.hpp")] + [os.path.join(ROOT, "include", "ea.h")]
+SOURCES = [os.path.join(CSRC, f) for f in ("ea_kernels.hip", "ea_half_c1.hip", "ea_half_c2.hip", "ea_half_c4.hip",
+                                            "ea_half_c8.hip", "ea_toy.hip", "ea_api.cpp")]
+HEADERS = [os.path.join(CSRC, f) for f in ("ea_device.hpp", "ea_launch.hpp", "ea_round.hpp")] + \
+    [os.path.join(ROOT, "include", "ea.h")]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-ffp-contract=off", "-fno-fast-math",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
@@ -28,9 +30,22 @@ FLAGS = [
 
 
 def build(verbose: bool = False, extra=()) -> str:
-    """Compile the library (always); returns its path."""
+    """Compile the library (always): each source to an object, in parallel,
+    then one link; returns its path."""
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    jobs = []
+    for src in SOURCES:
+        obj = os.path.join(objdir, os.path.basename(src) + ".o")
+        cmd = [HIPCC, *FLAGS, *extra, "-c", src, "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        jobs.append((cmd, obj, subprocess.Popen(cmd)))
+    failed = [cmd for cmd, _, p in jobs if p.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, failed[0])
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, *extra, *SOURCES, "-o", tmp]
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *[o for _, o, _ in jobs], "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

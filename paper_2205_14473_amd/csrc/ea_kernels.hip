@@ -1,1016 +1,11 @@
-// ea_kernels.hip -- HIP kernels of one Efficient-Adam round for gfx950.
-//
-// Work decomposition.  A tile is C chunks of 256 elements; a wave64 holds a
-// tile of one vector, four consecutive elements per lane.  Bucket norms are
-// reduced inside the wave (no LDS, no barrier); codes are bit-plane packed
-// with one ballot per 64-element plane word.
-//
-// The fused round (step_kernel) gives a block K consecutive tiles and one
-// wave per worker: each wave compresses its worker on the block's tiles and
-// hands the dequantized values over through LDS; then wave k adds the
-// handoffs of tile k in ascending worker order and runs the server's Adam,
-// quantization and the update of x on that tile (Algorithms 1-2, Section IV).
-// The split calls use blocks of 4 independent waves, one tile each.
-//
-// Every kernel is a template over the quantizer traits of both sides and the
-// Adam placement: QRt / placement -1 give the generic kernels used for any
-// configuration, QCt<...> the specialized ones for common shapes.  Tiles
-// that lie wholly inside d go to kernels without per-element bounds checks.
-#include "ea_launch.hpp"
+// ea_kernels.hip -- the generic and fully specialized fused-round kernels,
+// the split calls' kernels, and the launchers (dispatch to the kernel that
+// matches a configuration).  The round itself is in ea_round.hpp.
+#include "ea_round.hpp"
 
 namespace ea {
 
 namespace {
-
-// Largest number of waves in a block of the fused round (one worker each):
-// wide tiles need more registers per wave, so their blocks are narrower.
-#ifndef EA_WIDE_TILE_WAVES
-#define EA_WIDE_TILE_WAVES 8
-#endif
-#ifndef EA_NARROW_TILE_WAVES
-#define EA_NARROW_TILE_WAVES 16
-#endif
-#ifndef EA_ROUND_MIN_WAVES
-#define EA_ROUND_MIN_WAVES 5
-#endif
-#ifndef EA_EDGE_MIN_WAVES
-#define EA_EDGE_MIN_WAVES 5
-#endif
-__host__ __device__ constexpr int max_round_waves(int C)
-{
-    return C <= 2 ? EA_NARROW_TILE_WAVES : (C == 4 ? 8 : EA_WIDE_TILE_WAVES);
-}
-
-// Tiles per block of the fused round.  Lean kernels (whole tiles, Adam at
-// the server) take two consecutive tiles per block; the others one.
-#ifndef EA_TILES_PER_BLOCK
-#define EA_TILES_PER_BLOCK 2
-#endif
-__host__ __device__ constexpr int round_tiles_per_block(int C, bool lean)
-{
-    return C <= 2 && lean ? EA_TILES_PER_BLOCK : 1;
-}
-
-// Minimum waves per SIMD the compiler must leave room for (caps VGPRs).
-// Kernels over whole tiles with Adam at the server have no per-element
-// bounds checks and no worker moments, and need fewer registers than the
-// others.
-#ifndef EA_C4_MIN_WAVES
-#define EA_C4_MIN_WAVES 1
-#endif
-#ifndef EA_C8_MIN_WAVES
-#define EA_C8_MIN_WAVES 3
-#endif
-__host__ __device__ constexpr int round_min_waves(int C, bool lean)
-{
-    return C <= 2 ? (lean ? EA_ROUND_MIN_WAVES : EA_EDGE_MIN_WAVES)
-                  : (lean ? (C == 4 ? EA_C4_MIN_WAVES : EA_C8_MIN_WAVES) : 1);
-}
-
-// Number of valid elements among a lane's float4 at element n.
-__device__ __forceinline__ int nvalid4(int64_t n, int64_t d)
-{
-    const int64_t r = d - n;
-    return r <= 0 ? 0 : (r >= 4 ? 4 : (int)r);
-}
-
-template <int PL>
-__device__ __forceinline__ int placement_of(const StepArgs& a)
-{
-    return PL < 0 ? a.placement : PL;
-}
-
-// The launch's arguments with the step taken from the device when the round
-// reads it there (a.t_dev), and lr, beta2 from the schedule at that step
-// (Assumption 2: alpha/sqrt(T), 1 - theta/T; step decay: alpha * factor^k,
-// k = (t-1)/period, factor^k by square-and-multiply from the lowest bit).
-__device__ __forceinline__ StepArgs with_step(const StepArgs& in)
-{
-    StepArgs a = in;
-    if (a.t_dev == nullptr) return a;
-    const uint32_t t = *a.t_dev;
-    a.t = t;
-    if (a.sched_kind == EA_SCHED_ASSUMPTION2) {
-        const float Tf = (float)a.sched_T;
-        a.lr = a.sched_alpha / sqrtf(Tf);
-        a.beta2 = 1.0f - a.sched_theta / Tf;
-    } else if (a.sched_kind == EA_SCHED_STEP_DECAY) {
-        int64_t k = ((int64_t)t - 1) / a.sched_period;
-        float r = 1.0f, b = a.sched_factor;
-        while (k > 0) {
-            if (k & 1) r = r * b;
-            b = b * b;
-            k >>= 1;
-        }
-        a.lr = a.sched_alpha * r;
-    }
-    return a;
-}
-
-// ---------------------------------------------------------------------------
-// Quantize one tile: scales (reduced per bucket inside the wave, or given for
-// a one-bucket quantizer), codes, bit-plane packing and the dequantized
-// values.  codes/scales point at the start of the message.  The code words go
-// to `sink`, which the caller opens at the tile's first word (message_sink)
-// and flushes; consecutive tiles may share one sink, since their words are
-// consecutive in the message.
-// ---------------------------------------------------------------------------
-template <class QT>
-__device__ __forceinline__ WordSink message_sink(const QDev& q, uint64_t* codes, int64_t base)
-{
-    WordSink sink;
-    sink.out = codes + (base >> 8) * 4 * QT::bits(q);
-    sink.lo = 0u;
-    sink.hi = 0u;
-    sink.filled = 0;
-    return sink;
-}
-
-// Sparsifier tuning: how many of each lane's largest keys a first threshold
-// search runs on (0: none, 1 to 3), and whether the searches skip the bits
-// that all lane maxima share (1).
-#ifndef EA_SPARSE_SUBSET
-#define EA_SPARSE_SUBSET 3
-#endif
-#ifndef EA_SPARSE_PREFIX
-#define EA_SPARSE_PREFIX 1
-#endif
-
-// Threshold search over values the wave counts with count(c) = how many are
-// >= c (non-increasing in c): the largest T with count(T) >= kk, built bit by
-// bit from `top` down above a prefix T0 whose bits from `top` down are zero
-// and which the answer is known to share; or, as soon as some accepted
-// candidate is reached by exactly kk values, that candidate with exact set.
-// Each step is one ballot per counted value slot; the loop is kept rolled
-// (unrolling it measured no faster and multiplies the code).
-template <class Count>
-__device__ __forceinline__ uint32_t bit_select(const Count& count, uint32_t kk, int top, uint32_t T0, bool& exact)
-{
-    uint32_t T = T0;
-    exact = false;
-#pragma nounroll
-    for (int bit = top; bit >= 0; --bit) {
-        const uint32_t cand = T | (1u << bit);
-        const uint32_t n = count(cand);
-        if (n >= kk) {
-            T = cand;
-            if (n == kk) {
-                exact = true;
-                break;
-            }
-        }
-    }
-    return T;
-}
-
-__device__ __forceinline__ uint32_t wave_count(bool pred)
-{
-    return (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(pred));
-}
-
-// Bitwise OR and AND of a value over the wave (same steps as wave_max).
-__device__ __forceinline__ void wave_or_and(uint32_t v, uint32_t& o, uint32_t& a)
-{
-    o = v;
-    a = v;
-    o |= dpp<kDppXor1>(o);
-    a &= dpp<kDppXor1>(a);
-    o |= dpp<kDppXor2>(o);
-    a &= dpp<kDppXor2>(a);
-    o |= dpp<kDppHalfMirror>(o);
-    a &= dpp<kDppHalfMirror>(a);
-    o |= dpp<kDppRowMirror>(o);
-    a &= dpp<kDppRowMirror>(a);
-    uint32_t x, y;
-    row_swap16(o, x, y);
-    o = x | y;
-    row_swap16(a, x, y);
-    a = x & y;
-    row_swap32(o, x, y);
-    o = x | y;
-    row_swap32(a, x, y);
-    a = x & y;
-}
-
-// Definition 3 sparsifiers (TOPK, RANDK) on one tile.  Each bucket keeps
-// its k = min(keep, n) highest-ranked elements by a 32-bit key, larger keys
-// first and lower element indices first among equal keys: the magnitude's
-// bit pattern (TOPK) or the element's 24-bit draw word (RANDK).
-//
-// The k-th largest key T is found by a bitwise search (bit_select) that
-// counts with ballots; the search is the costly part, so three things cut its
-// steps and ballots.  (1) For k <= 64, T lies between the smallest and the
-// largest lane maximum, so the search starts below the bits all lane maxima
-// share (for magnitudes, typically the sign and most of the exponent).  (2) It first runs on each lane's three largest keys only (3
-// ballots a step instead of 4 per chunk) and keeps that answer when a full
-// count confirms it; else it runs again over every key.  (3) It stops as
-// soon as exactly k keys reach a candidate, which then splits the bucket
-// without ties.  Otherwise the keys equal to T are ranked by element index
-// (element n = 256c + 4l + s comes after every element of lower chunks, of
-// lower lanes of its chunk, and of lower slots of its lane).  The kept
-// values are listed in element order at positions counted the same way.
-// Elements past d get key 0 and the highest indices, so they rank below
-// every element of the vector and are never kept.
-template <int C, bool FULL, class QT>
-__device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C], int64_t base, int nch, int64_t d,
-                                              uint32_t k0, uint32_t k1, uint32_t step, uint32_t sid,
-                                              float* __restrict__ vals, WordSink& sink, float4 (&deq)[C])
-{
-    const int lane = lane_id();
-    const int cpb = QT::cpb(q);
-    const bool topk = QT::kind(q) == Q_TOPK;
-    const int top = topk ? 31 : 23;   // keys below 2^31 (TOPK) or 2^24 (RANDK)
-    if (FULL) nch = C;
-
-    uint32_t key[C][4];
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        const int nv = FULL ? 4 : (ch < nch ? nvalid4(n, d) : 0);
-        uint4 r = make_uint4(0u, 0u, 0u, 0u);
-        if (!topk && (FULL || ch < nch)) {
-            const uint64_t j = (uint64_t)n >> 2;
-            r = philox10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), step, sid), k0, k1);
-        }
-        const uint32_t rr[4] = {r.x, r.y, r.z, r.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const uint32_t kv = topk ? (__float_as_uint(comp(p[ch], k)) & 0x7FFFFFFFu) : (rr[k] >> 8);
-            key[ch][k] = (FULL || k < nv) ? kv : 0u;
-        }
-        deq[ch] = zero4();
-    }
-
-    const int64_t chunk0 = base >> 8;
-#pragma unroll
-    for (int b0 = 0; b0 < C; ++b0) {
-        if ((b0 & (cpb - 1)) != 0) continue;
-        if (!FULL && b0 >= nch) continue;
-        const int64_t e0 = base + (int64_t)b0 * kChunk;
-        const int64_t nb = FULL ? q.B : ((d - e0) < q.B ? (d - e0) : q.B);
-        const uint32_t kk = (uint32_t)(nb < q.keep ? nb : q.keep);
-
-        // Threshold T: the kk-th largest key of the bucket.
-        const auto count_all = [&](uint32_t c) {
-            uint32_t n = 0u;
-#pragma unroll
-            for (int j = 0; j < C; ++j) {
-                if (j < b0 || j >= b0 + cpb) continue;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) n += wave_count(key[j][k] >= c);
-            }
-            return n;
-        };
-        uint32_t T = 0u, gt = 0u;
-        bool exact = false, found = false, have_gt = false;
-        // The lanes' largest keys m[0] (and next largest m[1], m[2]).
-        uint32_t m[3] = {0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < C; ++j) {
-            if (j < b0 || j >= b0 + cpb) continue;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t x = key[j][k];
-                if (EA_SPARSE_SUBSET > 2) m[2] = max(m[2], min(m[1], x));
-                if (EA_SPARSE_SUBSET > 1) m[1] = max(m[1], min(m[0], x));
-                m[0] = max(m[0], x);
-            }
-        }
-        // With kk <= 64 the threshold lies between the smallest and largest
-        // lane maximum (64 keys reach the smallest), so it has the bits that
-        // every lane maximum shares above the highest bit where they differ.
-        int hi = top;
-        uint32_t prefix = 0u;
-        if (EA_SPARSE_PREFIX && kk <= (uint32_t)kWave) {
-            uint32_t o, n;
-            wave_or_and(m[0], o, n);
-            o = (uint32_t)__builtin_amdgcn_readfirstlane((int)o);
-            n = (uint32_t)__builtin_amdgcn_readfirstlane((int)n);
-            // bits above h: all of them for h < 0, none for h >= 31
-            const auto above = [](int h) { return h < 0 ? 0xFFFFFFFFu : (h >= 31 ? 0u : ~((2u << h) - 1u)); };
-            hi = o == n ? -1 : 31 - __builtin_clz(o ^ n);
-            if (hi > top) hi = top;
-            prefix = n & above(hi);
-        }
-        if (EA_SPARSE_SUBSET > 0 && kk <= (uint32_t)(EA_SPARSE_SUBSET * kWave)) {
-            // First on the keys that are among their lane's EA_SPARSE_SUBSET
-            // largest.  Its answer Tr holds for the bucket when the counts
-            // agree: every key above Tr is among them (Tr is then the kk-th
-            // largest of all), or, when exactly kk of them reach Tr, exactly
-            // kk keys of the bucket do.
-            const auto count_sub = [&](uint32_t c) {
-                uint32_t n = 0u;
-#pragma unroll
-                for (int r = 0; r < EA_SPARSE_SUBSET; ++r) n += wave_count(m[r] >= c);
-                return n;
-            };
-            bool er;
-            const uint32_t Tr = bit_select(count_sub, kk, hi, prefix, er);
-            if (er) {
-                found = exact = count_all(Tr) == kk;
-            } else {
-                gt = count_all(Tr + 1u);
-                found = have_gt = gt == count_sub(Tr + 1u);
-            }
-            T = Tr;
-        }
-        if (!found) T = bit_select(count_all, kk, hi, prefix, exact);
-
-        // Kept flags, bit 4j + k of a lane for its element in chunk j, slot k.
-        uint32_t kbits = 0u;
-        if (exact) {
-#pragma unroll
-            for (int j = 0; j < C; ++j) {
-                if (j < b0 || j >= b0 + cpb) continue;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) kbits |= (key[j][k] >= T ? 1u : 0u) << (4 * j + k);
-            }
-        } else {
-            if (!have_gt) {
-                gt = 0u;
-#pragma unroll
-                for (int j = 0; j < C; ++j) {
-                    if (j < b0 || j >= b0 + cpb) continue;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        gt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key[j][k] > T));
-                }
-            }
-            const uint32_t need = kk - gt;
-            uint32_t before = 0;
-#pragma unroll
-            for (int j = 0; j < C; ++j) {
-                if (j < b0 || j >= b0 + cpb) continue;
-                uint32_t below = 0, tot = 0;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint64_t em = __builtin_amdgcn_ballot_w64(key[j][k] == T);
-                    below += lanes_below(em);
-                    tot += (uint32_t)__builtin_popcountll(em);
-                }
-                uint32_t own = 0;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const bool eq = key[j][k] == T;
-                    const bool kept = key[j][k] > T || (eq && before + below + own < need);
-                    kbits |= (kept ? 1u : 0u) << (4 * j + k);
-                    own += eq ? 1u : 0u;
-                }
-                before += tot;
-            }
-        }
-
-        // Code words, values in element order, and the dequantized tile.  A
-        // plain store: the caches merge the bucket's scattered 4-byte values.
-        float* vb = vals + ((chunk0 + b0) >> QT::cpb_shift(q)) * (int64_t)q.keep;
-        uint32_t before = 0;
-#pragma unroll
-        for (int j = 0; j < C; ++j) {
-            if (j < b0 || j >= b0 + cpb) continue;
-            if (!FULL && j >= nch) continue;
-            uint64_t km[4];
-            uint32_t below = 0, tot = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                km[k] = __builtin_amdgcn_ballot_w64(((kbits >> (4 * j + k)) & 1u) != 0u);
-                below += lanes_below(km[k]);
-                tot += (uint32_t)__builtin_popcountll(km[k]);
-            }
-            uint32_t own = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const bool kept = ((kbits >> (4 * j + k)) & 1u) != 0u;
-                const float x = comp(p[j], k);
-                const uint32_t pos = before + below + own;   // < kk by construction; guarded all the same
-                if (kept && pos < (uint32_t)q.keep) vb[pos] = x;
-                own += kept ? 1u : 0u;
-                set_comp(deq[j], k, kept ? x : 0.0f);
-                sink.put(km[k]);
-            }
-            before += tot;
-        }
-        // A bucket shorter than keep: the remaining value slots are zero.
-        if (!FULL)
-            for (uint32_t sl = kk + (uint32_t)lane; sl < (uint32_t)q.keep; sl += kWave) vb[sl] = 0.0f;
-    }
-}
-
-template <int C, bool FULL, class QT>
-__device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, const float4 (&p)[C],
-                                              int64_t base, int nch, int64_t d, uint32_t k0, uint32_t k1,
-                                              uint32_t step, uint32_t sid, float given_scale,
-                                              uint64_t* __restrict__ codes, float* __restrict__ scales,
-                                              WordSink& sink, float4 (&deq)[C])
-{
-    if (is_sparse<QT>(q)) {
-        sparsify_tile<C, FULL, QT>(q, p, base, nch, d, k0, k1, step, sid, scales, sink, deq);
-        return;
-    }
-    const int lane = lane_id();
-    const int kind = QT::kind(q);
-    const int norm = QT::norm(q);
-    const int cpb = QT::cpb(q);
-    const int bits = QT::bits(q);
-    if (FULL) nch = C;
-
-    const int64_t chunk0 = base >> 8;   // first chunk of the tile (tiles start on bucket boundaries)
-    float s[C];
-    if (has_scale<QT>(q)) {
-        if (cpb == 0) {
-#pragma unroll
-            for (int ch = 0; ch < C; ++ch) s[ch] = given_scale;
-        } else {
-            Partial part[C];
-#pragma unroll
-            for (int ch = 0; ch < C; ++ch) {
-                part[ch].sum = 0.0;
-                part[ch].mx = 0.0f;
-                if (ch < nch)
-                    partial_add4(part[ch], norm, p[ch], FULL ? 4 : nvalid4(base + ch * kChunk + 4 * lane, d));
-            }
-#pragma unroll
-            for (int ch = 0; ch < C; ++ch) {
-                if ((ch & (cpb - 1)) == 0) {
-                    if (ch < nch) {
-                        Partial tot;
-                        tot.sum = 0.0;
-                        tot.mx = 0.0f;
-#pragma unroll
-                        for (int j = 0; j < C; ++j) {
-                            if (j >= ch && j < ch + cpb) {
-                                tot.sum += part[j].sum;
-                                tot.mx = fmaxf(tot.mx, part[j].mx);
-                            }
-                        }
-                        const int64_t b0 = base + (int64_t)ch * kChunk;
-                        const int64_t nb = FULL ? q.B : ((d - b0) < q.B ? (d - b0) : q.B);
-                        const double S = norm == S_MAX ? 0.0 : wave_sum(tot.sum);
-                        const float M = norm == S_MAX ? wave_max(tot.mx) : 0.0f;
-                        s[ch] = scale_from(norm, S, M, nb);
-                        // A plain store: the caches merge the 4-byte scales of
-                        // neighbouring tiles, where streaming stores reach HBM
-                        // one partial line at a time.
-                        if (lane == 0) scales[(chunk0 + ch) >> QT::cpb_shift(q)] = s[ch];
-                    } else {
-                        s[ch] = 0.0f;
-                    }
-                } else {
-                    s[ch] = s[ch > 0 ? ch - 1 : 0];
-                }
-            }
-        }
-    } else {
-#pragma unroll
-        for (int ch = 0; ch < C; ++ch) s[ch] = 1.0f;
-    }
-
-    const bool gated = scale_gated<QT>(q);
-    if (kind == Q_NONE) {
-        float* raw = reinterpret_cast<float*>(codes);
-#pragma unroll
-        for (int ch = 0; ch < C; ++ch) {
-            deq[ch] = p[ch];
-            if (FULL || ch < nch) st4<false>(raw, base + (int64_t)ch * kChunk + 4 * lane, d, p[ch]);
-        }
-        return;
-    }
-    // Codes are produced slot by slot and each code plane goes straight into
-    // a ballot word, in message word order (4*chunk + slot)*bits + plane.
-    // The scale, its reciprocal and the gate are wave-uniform and computed
-    // once per bucket.
-    float sc = 0.0f, inv = 0.0f;
-    bool ok = true;
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        const int nv = FULL ? 4 : (ch < nch ? nvalid4(n, d) : 0);
-        if (ch == 0 || (cpb != 0 && (ch & (cpb - 1)) == 0)) {
-            sc = uniform(s[ch]);
-            ok = !gated || (sc > 0.0f && !isinf(sc));
-            inv = 1.0f / sc;
-        }
-        if (!ok) {
-            // Zero or non-finite scale (uniform over the wave): the chunk is
-            // sent as zero codes and dequantizes to zero.
-            const uint32_t zc = zero_code_of<QT>(q);
-            deq[ch] = zero4();
-            if (FULL || ch < nch) {
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const bool valid = FULL || k < nv;
-                    for (int pl = 0; pl < bits; ++pl)
-                        sink.put(__builtin_amdgcn_ballot_w64(valid && ((zc >> pl) & 1u) != 0u));
-                }
-            }
-            continue;
-        }
-        uint4 r = make_uint4(0u, 0u, 0u, 0u);
-        if (kind == Q_STOCH && (FULL || ch < nch)) {
-            const uint64_t j = (uint64_t)n >> 2;
-            r = philox10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), step, sid), k0, k1);
-        }
-        const uint32_t rr[4] = {r.x, r.y, r.z, r.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const float x = comp(p[ch], k);
-            uint32_t cc = code_of<QT>(q, x, inv, rr[k]);
-            float dv = deq_of<QT>(q, lut, cc, x, sc);
-            if (!FULL && k >= nv) {
-                cc = 0u;
-                dv = 0.0f;
-            }
-            set_comp(deq[ch], k, dv);
-            if (FULL || ch < nch) {
-                if constexpr (QT::fixed) {
-                    // Codes are below 2^bits, so the top plane is a compare.
-#pragma unroll
-                    for (int pl = 0; pl < QT::bits(q); ++pl)
-                        sink.put(__builtin_amdgcn_ballot_w64(pl == QT::bits(q) - 1 ? cc >= (1u << pl)
-                                                                                    : ((cc >> pl) & 1u) != 0u));
-                } else {
-                    for (int pl = 0; pl < bits; ++pl)
-                        sink.put(__builtin_amdgcn_ballot_w64(((cc >> pl) & 1u) != 0u));
-                }
-            }
-        }
-    }
-}
-
-// Dequantize one tile of a message (the inverse of the code table).
-template <int C, class QT>
-__device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, const uint64_t* __restrict__ codes,
-                                             const float* __restrict__ scales, int64_t base, int nch, int64_t d,
-                                             float4 (&deq)[C])
-{
-    const int lane = lane_id();
-    const int bits = QT::bits(q);
-    if (is_sparse<QT>(q)) {
-        // Kept elements take their bucket's values in element order; the
-        // count of kept elements before a chunk restarts at each bucket.
-        uint32_t before = 0;
-#pragma unroll
-        for (int ch = 0; ch < C; ++ch) {
-            deq[ch] = zero4();
-            if (ch >= nch) continue;
-            const int64_t chunk = (base >> 8) + ch;
-            if ((chunk & (QT::cpb(q) - 1)) == 0) before = 0;
-            const uint64_t* w = codes + chunk * 4;
-            const float* vb = scales + (chunk >> QT::cpb_shift(q)) * (int64_t)q.keep;
-            uint64_t m[4];
-            uint32_t below = 0, tot = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                m[k] = w[k];
-                below += lanes_below(m[k]);
-                tot += (uint32_t)__builtin_popcountll(m[k]);
-            }
-            uint32_t own = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                // A mask with more than keep bits in a bucket (not a message
-                // this library wrote) reads no value past the bucket's slots.
-                const bool kept = ((m[k] >> lane) & 1u) != 0u;
-                const uint32_t pos = before + below + own;
-                set_comp(deq[ch], k, kept && pos < (uint32_t)q.keep ? vb[pos] : 0.0f);
-                own += kept ? 1u : 0u;
-            }
-            before += tot;
-        }
-        return;
-    }
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        deq[ch] = zero4();
-        if (ch >= nch) continue;
-        if (QT::kind(q) == Q_NONE) {
-            deq[ch] = ld4<false>(reinterpret_cast<const float*>(codes), n, d);
-            continue;
-        }
-        const int64_t chunk = (base >> 8) + ch;
-        float sc = 1.0f;
-        if (has_scale<QT>(q)) sc = scales[QT::cpb(q) == 0 ? 0 : (chunk >> QT::cpb_shift(q))];
-        sc = uniform(sc);
-        const bool ok = !scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc));
-        const uint64_t* w = codes + chunk * 4 * bits;
-        const int nv = nvalid4(n, d);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            uint32_t cc = 0;
-            for (int pl = 0; pl < bits; ++pl) cc |= (uint32_t)((w[k * bits + pl] >> lane) & 1u) << pl;
-            const float dv = ok ? deq_of<QT>(q, lut, cc, 0.0f, sc) : 0.0f;
-            set_comp(deq[ch], k, k < nv ? dv : 0.0f);
-        }
-    }
-}
-
-// Raw worker rows of one tile.
-template <int C>
-struct WorkerRows {
-    float4 g[C], e[C], m[C], v[C];
-};
-
-template <int C, bool VEC, bool FULL, int PL>
-__device__ __forceinline__ void load_worker(const StepArgs& a, const float* __restrict__ g,
-                                            const float* __restrict__ e, const float* __restrict__ mw,
-                                            const float* __restrict__ vw, int64_t base, int nch,
-                                            WorkerRows<C>& r)
-{
-    const int lane = lane_id();
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        if (!FULL && ch >= nch) {
-            r.g[ch] = r.e[ch] = r.m[ch] = r.v[ch] = zero4();
-            continue;
-        }
-        r.g[ch] = ld4<VEC, FULL>(g, n, a.d);
-        r.e[ch] = ld4<VEC, FULL>(e, n, a.d);
-        if (placement_of<PL>(a) == AT_WORKER) {
-            r.m[ch] = ld4<VEC, FULL>(mw, n, a.d);
-            r.v[ch] = ld4<VEC, FULL>(vw, n, a.d);
-        }
-    }
-}
-
-// p for a worker: g + e (Adam at the server) or lr*m/sqrt(v) + e after the
-// moment update (Adam at the workers); updated moments are left in r.
-template <int C, int PL>
-__device__ __forceinline__ void worker_p(const StepArgs& a, WorkerRows<C>& r, float4 (&p)[C])
-{
-    const float omb1 = 1.0f - a.beta1, omb2 = 1.0f - a.beta2;
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (placement_of<PL>(a) == AT_WORKER) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float gk = comp(r.g[ch], k);
-                const float vk = a.beta2 * comp(r.v[ch], k) + omb2 * (gk * gk);
-                const float mk = a.beta1 * comp(r.m[ch], k) + omb1 * gk;
-                set_comp(r.v[ch], k, vk);
-                set_comp(r.m[ch], k, mk);
-                const float uk = vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f;
-                set_comp(p[ch], k, uk + comp(r.e[ch], k));
-            }
-        } else {
-            p[ch] = add4(r.g[ch], r.e[ch]);
-        }
-    }
-}
-
-template <int C, bool VEC, bool FULL, int PL>
-__device__ __forceinline__ void store_moments(const StepArgs& a, float* __restrict__ mw, float* __restrict__ vw,
-                                              int64_t base, int nch, const WorkerRows<C>& r)
-{
-    if (placement_of<PL>(a) != AT_WORKER) return;
-    const int lane = lane_id();
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (!FULL && ch >= nch) continue;
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        st4<VEC, FULL>(mw, n, a.d, r.m[ch]);
-        st4<VEC, FULL>(vw, n, a.d, r.v[ch]);
-    }
-}
-
-// The server's rows of one tile: Adam moments (Adam at the server), the
-// server error and x.
-template <int C>
-struct ServerRows {
-    float4 m[C], v[C], e[C], x[C];
-};
-
-template <int C, bool VEC, bool FULL, int PL>
-__device__ __forceinline__ void load_server(const StepArgs& a, int64_t base, int nch, bool with_e, bool with_x,
-                                            ServerRows<C>& r)
-{
-    const int lane = lane_id();
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        r.m[ch] = r.v[ch] = r.e[ch] = r.x[ch] = zero4();
-        if (!FULL && ch >= nch) continue;
-        if (placement_of<PL>(a) == AT_SERVER) {
-            r.m[ch] = ld4<VEC, FULL>(a.m, n, a.d);
-            r.v[ch] = ld4<VEC, FULL>(a.v, n, a.d);
-        }
-        if (with_e) r.e[ch] = ld4<VEC, FULL>(a.e_s, n, a.d);
-        if (with_x) r.x[ch] = ld4<VEC, FULL>(a.x, n, a.d);
-    }
-}
-
-// Average of the dequantized sum: a division by N, done as a multiplication
-// by 1/N when N is a power of two (both are the correctly rounded x/N).
-__device__ __forceinline__ float avg_of(float x, float fN, float invN, bool pow2)
-{
-    return pow2 ? x * invN : x / fN;
-}
-
-// Server input from the worker sum: Adam (at the server) or the average.
-template <int C, bool VEC, bool FULL, int PL>
-__device__ __forceinline__ void server_input(const StepArgs& a, const float4 (&acc)[C], int64_t base, int nch,
-                                             ServerRows<C>& sr, float4 (&u)[C])
-{
-    const int lane = lane_id();
-    const float fN = (float)a.N;
-    const bool pow2 = (a.N & (a.N - 1)) == 0;
-    const float invN = 1.0f / fN;
-    const float omb1 = 1.0f - a.beta1, omb2 = 1.0f - a.beta2;
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        if (!FULL && ch >= nch) {
-            u[ch] = zero4();
-            continue;
-        }
-        float4 avg = make_float4(avg_of(acc[ch].x, fN, invN, pow2), avg_of(acc[ch].y, fN, invN, pow2),
-                                 avg_of(acc[ch].z, fN, invN, pow2), avg_of(acc[ch].w, fN, invN, pow2));
-        if (placement_of<PL>(a) == AT_SERVER) {
-            float4 mv = sr.m[ch];
-            float4 vv = sr.v[ch];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float gk = comp(avg, k);
-                const float vk = a.beta2 * comp(vv, k) + omb2 * (gk * gk);
-                const float mk = a.beta1 * comp(mv, k) + omb1 * gk;
-                set_comp(vv, k, vk);
-                set_comp(mv, k, mk);
-                set_comp(avg, k, vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f);
-            }
-            st4<VEC, FULL>(a.m, n, a.d, mv);
-            st4<VEC, FULL>(a.v, n, a.d, vv);
-        }
-        u[ch] = avg;
-    }
-}
-
-// Partial norm of a tile, reduced over the wave (one-bucket quantizers).
-template <int C>
-__device__ __forceinline__ double tile_partial(const QDev& q, const float4 (&p)[C], int64_t base, int nch,
-                                               int64_t d)
-{
-    Partial a;
-    a.sum = 0.0;
-    a.mx = 0.0f;
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch)
-        if (ch < nch) partial_add4(a, q.norm, p[ch], nvalid4(base + ch * kChunk + 4 * lane_id(), d));
-    return q.norm == S_MAX ? (double)wave_max(a.mx) : wave_sum(a.sum);
-}
-
-struct TilePos {
-    int64_t tile, base;
-    int nch;
-};
-
-template <int C>
-__device__ __forceinline__ bool tile_pos(const StepArgs& a, TilePos& t)
-{
-    t.tile = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x / kWave);
-    if (t.tile >= a.ntiles) return false;
-    t.base = t.tile * C * kChunk;
-    const int64_t rem = (a.d - t.base + kChunk - 1) / kChunk;
-    t.nch = rem < C ? (int)rem : C;
-    return true;
-}
-
-// ---------------------------------------------------------------------------
-// One worker's share of a tile: wave w compresses worker i and leaves its
-// dequantized values in the handoff slot.
-template <int C, bool VEC, bool FULL, int PL>
-__device__ __forceinline__ void worker_load(const StepArgs& a, const TilePos& t, int i, WorkerRows<C>& r)
-{
-    const bool atw = placement_of<PL>(a) == AT_WORKER;
-    const int64_t row = (int64_t)i * a.d;
-    load_worker<C, VEC, FULL, PL>(a, a.g + row, a.e_w + row, atw ? a.m_w + row : nullptr,
-                                  atw ? a.v_w + row : nullptr, t.base, t.nch, r);
-}
-
-template <int C, bool VEC, bool FULL, class QW, int PL>
-__device__ __forceinline__ void worker_compute(const StepArgs& a, const TilePos& t, const float* lut_w, int i,
-                                               WorkerRows<C>& r, WordSink& sink, float4* slot)
-{
-    const int lane = lane_id();
-    const bool wglobal = has_scale<QW>(a.qw) && QW::cpb(a.qw) == 0;
-    const bool atw = placement_of<PL>(a) == AT_WORKER;
-    const int64_t row = (int64_t)i * a.d;
-    float4 p[C], dq[C];
-    worker_p<C, PL>(a, r, p);
-    if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
-    const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
-    quantize_tile<C, FULL, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
-                               a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales, sink, dq);
-    float* e = a.e_w + row;
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (!FULL && ch >= t.nch) continue;
-        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        st4<VEC, FULL>(e, n, a.d, a.qw.ef ? sub4(p[ch], dq[ch]) : zero4());
-    }
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) slot[ch * kWave + lane] = dq[ch];
-}
-
-// Wave 0: add the cnt handoff slots of a group, in ascending worker order.
-template <int C>
-__device__ __forceinline__ void gather_group(const float4* slot, int cnt, float4 (&acc)[C])
-{
-    const int lane = lane_id();
-    for (int j = 0; j < cnt; ++j) {
-#pragma unroll
-        for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], slot[(j * C + ch) * kWave + lane]);
-    }
-}
-
-// Position of tile `tile` of C chunks.
-template <int C>
-__device__ __forceinline__ TilePos tile_at(const StepArgs& a, int64_t tile)
-{
-    TilePos t;
-    t.tile = tile;
-    t.base = tile * C * kChunk;
-    const int64_t rem = (a.d - t.base + kChunk - 1) / kChunk;
-    t.nch = rem < C ? (int)rem : C;
-    return t;
-}
-
-// Worker i on the block's nt consecutive tiles: the rows of all of them are
-// loaded first, so the later tiles' loads are in flight while the first is
-// compressed; the codes of the tiles leave through one sink, as one piece.
-// Tile k's dequantized values go to slots + (k*G + w)*C*64.
-template <int C, int K, bool VEC, bool FULL, class QW, int PL>
-__device__ __forceinline__ void worker_tiles(const StepArgs& a, const TilePos (&tp)[K], int nt, const float* lut_w,
-                                             int i, float4* slots, int G, int w)
-{
-    WorkerRows<C> r[K];
-#pragma unroll
-    for (int k = 0; k < K; ++k)
-        if (k < nt) worker_load<C, VEC, FULL, PL>(a, tp[k], i, r[k]);
-    WordSink sink = message_sink<QW>(a.qw, a.wcodes + (int64_t)i * a.qw.words, tp[0].base);
-#pragma unroll
-    for (int k = 0; k < K; ++k)
-        if (k < nt)
-            worker_compute<C, VEC, FULL, QW, PL>(a, tp[k], lut_w, i, r[k], sink,
-                                                 slots + ((int64_t)k * G + w) * C * kWave);
-    sink.flush();
-}
-
-// ---------------------------------------------------------------------------
-// The fused round on nt <= K consecutive tiles per block.  The block has
-// G = min(N, 16) waves.  Workers are taken in groups of G: wave w compresses
-// worker g0 + w on every tile of the block and hands its dequantized values
-// over through LDS.  Wave k then serves tile k: it adds the handoffs in
-// ascending worker order (the order of the average in Algorithm 1) and, after
-// the last group, runs the server side on its tile.  Short-lived per-worker
-// waves keep far more independent memory traffic in flight than one wave
-// looping over all workers, and serving the tiles on separate waves keeps the
-// server work off the workers' path.  The handoff is double-buffered over
-// groups, so one barrier per group suffices: a buffer is rewritten only after
-// the barrier that the serving waves reach once they have read the buffer's
-// previous group.  The last group is peeled off so that the serving waves can
-// issue the server's loads before the last barrier: their latency overlaps
-// the wait for the workers, without the loaded rows being live during the
-// earlier groups.
-// ---------------------------------------------------------------------------
-template <int C, int K, bool VEC, bool FULL, class QW, class QS, int PL>
-__device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, int nt, const float* lut_w,
-                                            const float* lut_s, float4* xfer, int G)
-{
-    const int lane = lane_id();
-    const int w = (int)(threadIdx.x / kWave);
-    const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
-
-    TilePos tp[K];
-#pragma unroll
-    for (int k = 0; k < K; ++k) tp[k] = tile_at<C>(a, tile0 + k);
-
-    float4 acc[C];
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
-
-    // Handoff layout: [group buffer][tile][wave][chunk][lane].
-    const int64_t per_buf = (int64_t)K * G * C * kWave;
-    int buf = 0, g0 = 0;
-    for (; g0 + G < a.N; g0 += G, buf ^= 1) {
-        float4* slots = xfer + buf * per_buf;
-        worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
-        __syncthreads();
-        if (w < nt) gather_group<C>(slots + (int64_t)w * G * C * kWave, G, acc);
-    }
-    float4* slots = xfer + buf * per_buf;
-    if (g0 + w < a.N) worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
-    const TilePos t = tile_at<C>(a, tile0 + (w < nt ? w : 0));
-    ServerRows<C> sr;
-    if (w < nt) load_server<C, VEC, FULL, PL>(a, t.base, t.nch, true, !sglobal, sr);
-    __syncthreads();
-    if (w >= nt) return;
-    gather_group<C>(slots + (int64_t)w * G * C * kWave, a.N - g0, acc);
-
-    float4 u[C], q[C], dq[C];
-    server_input<C, VEC, FULL, PL>(a, acc, t.base, t.nch, sr, u);
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) q[ch] = add4(u[ch], sr.e[ch]);
-    if (sglobal) {
-#pragma unroll
-        for (int ch = 0; ch < C; ++ch)
-            if (FULL || ch < t.nch) st4<VEC, FULL>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
-        const double part = tile_partial<C>(a.qs, q, t.base, t.nch, a.d);
-        if (lane == 0) a.spart[t.tile] = part;
-        return;
-    }
-    WordSink sink = message_sink<QS>(a.qs, a.scodes, t.base);
-    quantize_tile<C, FULL, QS>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, 0.0f, a.scodes,
-                               a.sscales, sink, dq);
-    sink.flush();
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (!FULL && ch >= t.nch) continue;
-        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        st4<VEC, FULL>(a.e_s, n, a.d, a.qs.ef ? sub4(q[ch], dq[ch]) : zero4());
-        st4<VEC, FULL>(a.x, n, a.d, sub4(sr.x[ch], dq[ch]));
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Kernels
-// ---------------------------------------------------------------------------
-
-// Floats of the code-table region of a fused-round block with G waves: room
-// for both block-wide tables or for two 64-entry tables per wave.
-__host__ __device__ constexpr int table_floats(int G)
-{
-    return 2 * kLutSize > 2 * kWave * G ? 2 * kLutSize : 2 * kWave * G;
-}
-
-// Dynamic LDS of a fused-round block with G waves: the code tables plus the
-// handoff of G workers' tiles (double-buffered when N > G).
-inline size_t round_lds_bytes(int N, int C, int G, int K)
-{
-    const int nbuf = N > G ? 2 : 1;
-    return table_floats(G) * sizeof(float) + (size_t)nbuf * K * G * C * kWave * sizeof(float4);
-}
-
-// Waves per block: one per worker up to the tile's limit, fewer if the LDS
-// would exceed what a block may use.
-inline int round_waves(int N, int C, int K, size_t lds_limit)
-{
-    int G = N < max_round_waves(C) ? N : max_round_waves(C);
-    while (G > 1 && round_lds_bytes(N, C, G, K) > lds_limit) G = (G + 1) / 2;
-    return G;
-}
-
-// Per-block LDS limit of the current device (queried once per device).
-size_t lds_limit_bytes()
-{
-    static size_t cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 64 * 1024;
-    if (cached[dev] == 0) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
-            v = 64 * 1024;
-        cached[dev] = (size_t)v;
-    }
-    return cached[dev];
-}
-
-// The fused round.  With a one-bucket Q_w the worker scales are read from
-// wscales (computed beforehand); with a one-bucket Q_s the block stops after
-// the server input, which it leaves in ubuf with per-tile partial norms.
-//
-// FULL kernels (rows 16-byte aligned) take the tiles that lie wholly inside d
-// and carry no bounds checks; the others take any tile.  A launch covers
-// tiles [a.tile0, a.tile1); block b works on the K tiles from
-// a.tile0 + b*K.
-template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
-__global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
-    StepArgs args)
-{
-    const StepArgs a = with_step(args);
-    static_assert(!FULL || VEC, "whole-tile kernels need aligned rows");
-    extern __shared__ float4 smem[];
-    const int G = (int)(blockDim.x / kWave);
-    float* lut_w;
-    float* lut_s;
-    if constexpr (WaveTable<QW>::value && WaveTable<QS>::value) {
-        float* tab = reinterpret_cast<float*>(smem) + (threadIdx.x / kWave) * 2 * kWave;
-        fill_wave_table<QW>(a.qw, tab);
-        fill_wave_table<QS>(a.qs, tab + kWave);
-        lut_w = tab;
-        lut_s = tab + kWave;
-    } else {
-        lut_w = reinterpret_cast<float*>(smem);
-        lut_s = lut_w + kLutSize;
-        fill_lut(a.qw, lut_w);
-        fill_lut(a.qs, lut_s);
-        __syncthreads();
-    }
-    float4* xfer = smem + table_floats(G) / 4;
-    constexpr int K = round_tiles_per_block(C, FULL && PL == AT_SERVER);
-    const int64_t first = a.tile0 + (int64_t)blockIdx.x * K;
-    const int64_t left = a.tile1 - first;
-    round_tiles<C, K, VEC, FULL, QW, QS, PL>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G);
-}
 
 // Per-tile partial norms of the worker inputs p for workers [i0, i1), without
 // writing any state (one-bucket Q_w).  Rows are [i - i0][d] from a.g etc.
@@ -1275,19 +270,37 @@ const Special* find_special(const StepArgs& a, int C)
     return nullptr;
 }
 
+// A kernel specialized for the worker quantizer, when one matches: whole
+// tiles of one worker bucket each.
+const HalfKernel* find_half(const StepArgs& a, int C)
+{
+    if (a.qw.cpb != C) return nullptr;
+    int n = 0;
+    const HalfKernel* t = C == 1 ? half_kernels_c1(&n) : C == 2 ? half_kernels_c2(&n)
+                        : C == 4 ? half_kernels_c4(&n) : C == 8 ? half_kernels_c8(&n) : nullptr;
+    for (int i = 0; i < n; ++i) {
+        const HalfKernel& h = t[i];
+        if (h.C == C && h.wkind == a.qw.kind && h.wbits == a.qw.bits && h.wnorm == a.qw.norm && h.wcpb == a.qw.cpb)
+            return &h;
+    }
+    return nullptr;
+}
+
 }  // namespace
 
-// Whole tiles go to a kernel without bounds checks and the ragged last tile
-// to a checked one, both specialized when one matches the configuration;
-// every tile of rows that are not 16-byte aligned goes to the generic checked
-// kernel.
+// Whole tiles go to a kernel without bounds checks: one specialized for both
+// quantizers and the placement when one matches, else one specialized for
+// the worker quantizer, else the generic one.  The ragged last tile goes to a
+// checked kernel, specialized in the first case.  Every tile of rows that are
+// not 16-byte aligned goes to the generic checked kernel.
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
     const size_t limit = lds_limit_bytes();
     const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) : 0;
     const Special* sp = vec ? find_special(a, C) : nullptr;
+    const HalfKernel* hk = vec && !sp ? find_half(a, C) : nullptr;
     if (nfull > 0) {
-        const int K = sp ? sp->tiles : round_tiles_per_block(C, false);
+        const int K = sp ? sp->tiles : hk ? hk->tiles : round_tiles_per_block(C, false);
         const int G = round_waves(a.N, C, K, limit);
         StepArgs b = a;
         b.tile0 = 0;
@@ -1296,6 +309,8 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
         const size_t lds = round_lds_bytes(a.N, C, G, K);
         if (sp) {
             hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
+        } else if (hk) {
+            hipLaunchKernelGGL(hk->kernel, grid, block, lds, s, b);
         } else {
             switch (C) {
             case 1: hipLaunchKernelGGL((step_kernel<1, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
@@ -1329,11 +344,6 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
         return hipGetLastError();
     }
     return hipSuccess;
-}
-
-bool has_special_step(const StepArgs& a, int C, bool vec)
-{
-    return vec && find_special(a, C) != nullptr;
 }
 
 hipError_t launch_worker_partials(const StepArgs& a, int C, bool vec, int i0, int i1, hipStream_t s)

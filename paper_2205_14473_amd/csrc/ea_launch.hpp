@@ -1,5 +1,5 @@
 // ea_launch.hpp -- kernel argument block and launchers shared by the C ABI
-// (ea_api.cpp) and the kernels (ea_kernels.hip).
+// (ea_api.cpp) and the kernels (ea_kernels.hip, ea_half_c*.hip, ea_toy.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -52,8 +52,20 @@ struct StepArgs {
 
 // Launchers; C = chunks per tile (1..8), vec = rows are 16-byte aligned.
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s);
-// True when launch_step uses a kernel specialized for this configuration.
-bool has_special_step(const StepArgs& a, int C, bool vec);
+
+// Fused-round kernels specialized for the worker quantizer only (kind, code
+// bits, norm and chunks per bucket fixed; the server quantizer and the Adam
+// placement read at run time), for whole tiles of C = chunks-per-bucket
+// chunks.  One table per C, each compiled in its own translation unit.
+struct HalfKernel {
+    int C, wkind, wbits, wnorm, wcpb;
+    void (*kernel)(StepArgs);
+    int tiles;                // tiles per block
+};
+const HalfKernel* half_kernels_c1(int* n);
+const HalfKernel* half_kernels_c2(int* n);
+const HalfKernel* half_kernels_c4(int* n);
+const HalfKernel* half_kernels_c8(int* n);
 hipError_t launch_worker_partials(const StepArgs& a, int C, bool vec, int i0, int i1, hipStream_t s);
 hipError_t launch_server_partials(const StepArgs& a, int C, bool vec, hipStream_t s);
 hipError_t launch_finalize(const double* part, int64_t ntiles, int32_t norm, int64_t n, float* out,

@@ -1,0 +1,62 @@
+"""GPU parity of the fused-round kernels specialized for the worker quantizer
+only (the server quantizer and the Adam placement read at run time): every
+worker quantizer of those tables (scaled sign; stochastic 1/2/4/8-bit with L2
+or max-norm scale; top-k; random-k) at every bucket size 256 to 2048, paired
+with a different server quantizer whose bucket is no larger, in both
+placements.  Sizes hold several whole tiles (the specialized launch) and a
+ragged tail (the generic edge launch); one-chunk tiles go two to a block, so
+odd and even tile counts both occur."""
+import pytest
+
+import oracle as O
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU-only host
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from parity_util import Pair, qfields  # noqa: E402
+
+WORKER = {
+    "sign": lambda b: qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 1, b),
+    "stoch1_l2": lambda b: qfields(O.Q_STOCH_UNIFORM, 1, O.SCALE_L2, 1, b),
+    "stoch1_max": lambda b: qfields(O.Q_STOCH_UNIFORM, 1, O.SCALE_MAX, 1, b),
+    "stoch2_l2": lambda b: qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_L2, 1, b),
+    "stoch2_max": lambda b: qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, 1, b),
+    "stoch4_l2": lambda b: qfields(O.Q_STOCH_UNIFORM, 4, O.SCALE_L2, 1, b),
+    "stoch4_max": lambda b: qfields(O.Q_STOCH_UNIFORM, 4, O.SCALE_MAX, 1, b),
+    "stoch8_l2": lambda b: qfields(O.Q_STOCH_UNIFORM, 8, O.SCALE_L2, 1, b),
+    "stoch8_max": lambda b: qfields(O.Q_STOCH_UNIFORM, 8, O.SCALE_MAX, 1, b),
+    "topk": lambda b: qfields(O.Q_TOPK, bucket=b, keep=b // 32 + 1),
+    "randk": lambda b: qfields(O.Q_RANDK, bucket=b, keep=b // 16),
+}
+# A server quantizer of another kind, bucket no larger than the worker's.
+SERVER = [
+    lambda b: qfields(O.Q_DET_UNIFORM, 3, bucket=b),
+    lambda b: qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, 1, max(256, b // 2)),
+    lambda b: qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 1, 256),
+    lambda b: qfields(O.Q_TOPK, bucket=b, keep=7),
+]
+
+
+def _grads(seed, t, N, d):
+    w = W.Workload("t", "t", d, N, None, None, 1, seed, "student_t")
+    return W.host_gradients(w, t, d=d)
+
+
+@pytest.mark.parametrize("bucket", [256, 512, 1024, 2048])
+@pytest.mark.parametrize("kind", list(WORKER))
+def test_worker_specialized_kernels(kind, bucket):
+    qw = WORKER[kind](bucket)
+    k = list(WORKER).index(kind)
+    qs = SERVER[k % len(SERVER)](bucket)
+    placement = O.ADAM_AT_SERVER if k % 2 == 0 else O.ADAM_AT_WORKER
+    tiles = 5 if bucket > 256 else 6          # one-chunk tiles: an even count, plus the tail
+    d = bucket * tiles + 100
+    pair = Pair(d, 5, qw, qs, placement, seed=11 + k)
+    for t in range(1, 4):
+        pair.step(t, _grads(11 + k, t, 5, d))
+    pair.check_tie_budget()
+    print(f"\n[parity] half {kind} bucket={bucket} placement={placement}: {pair.stats}", flush=True)
