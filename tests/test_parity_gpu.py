@@ -148,6 +148,17 @@ def test_two_tile_blocks_many_workers():
     _run(512 * 5, 20, SIGN(512), SIGN(512), O.ADAM_AT_SERVER, T=3)
 
 
+@pytest.mark.parametrize("N", [100, 1024])
+def test_many_workers(N):
+    """Many groups of workers per block (double-buffered handoff), up to the
+    largest N the library accepts: the specialized, worker-specialized and
+    generic kernels, both placements."""
+    d = 512 * 2 + 40 if N > 200 else 512 * 4 + 300
+    _run(d, N, STOCH(4, O.SCALE_L2, 512), STOCH(4, O.SCALE_L2, 512), O.ADAM_AT_SERVER, T=2)
+    _run(d, N, STOCH(4, O.SCALE_MAX, 512), SIGN(256), O.ADAM_AT_WORKER, T=2)
+    _run(d, N, qfields(O.Q_DET_UNIFORM, 2, bucket=512), SIGN(1024), O.ADAM_AT_SERVER, T=2)
+
+
 def test_zero_buckets_in_lean_kernels():
     """Buckets whose scale is zero take the wave-uniform branch of the
     specialized kernels (bert quantizers, Adam at the server)."""
