@@ -68,6 +68,15 @@ def test_toy_full_trajectory():
     print(f"\n[parity] toy: {pair.stats}", flush=True)
 
 
+@pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
+def test_bert_shape_100_step_trajectory(placement):
+    """The BERT workload's quantizers, N = 16 and ragged tail at reduced d,
+    compared after every step of a 100-step trajectory."""
+    d, N, qw, qs, gen = SHAPES["bert"]
+    pair = _run(d, N, qw, qs, placement, T=100, gen=gen)
+    assert pair.stats.steps == 100
+
+
 @pytest.mark.parametrize("split", [False, True], ids=["fused", "split"])
 @pytest.mark.parametrize("ex", ["ex1", "ex2"])
 def test_paper_toy_examples(ex, split):
