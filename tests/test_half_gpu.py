@@ -60,3 +60,15 @@ def test_worker_specialized_kernels(kind, bucket):
         pair.step(t, _grads(11 + k, t, 5, d))
     pair.check_tie_budget()
     print(f"\n[parity] half {kind} bucket={bucket} placement={placement}: {pair.stats}", flush=True)
+
+
+@pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
+def test_worker_specialized_with_one_bucket_server(placement):
+    """The server's one-bucket quantizer makes the fused round stop after the
+    server input (per-tile partial norms, then the finalize and server
+    kernels)."""
+    d = 512 * 7 + 32                    # rows 16-byte aligned: whole tiles take the specialized kernel
+    pair = Pair(d, 6, WORKER["stoch4_max"](512), qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 1, 0), placement, seed=3)
+    for t in range(1, 4):
+        pair.step(t, _grads(3, t, 6, d))
+    pair.check_tie_budget()
