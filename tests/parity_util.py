@@ -225,8 +225,8 @@ class Pair:
             close("v_w", rb.v_w.cpu().numpy(), st.v_w, s)
         if self.split and out.get("srv_in") is not None:
             close("u", rb.u.cpu().numpy(), out["srv_in"], s)
-        exact = (np.array_equal(rb.x.cpu().numpy(), st.x) and np.array_equal(rb.e_w.cpu().numpy(), st.e_w)
-                 and np.array_equal(rb.e_s.cpu().numpy(), st.e_s))
+        exact = (same_values(rb.x.cpu().numpy(), st.x) and same_values(rb.e_w.cpu().numpy(), st.e_w)
+                 and same_values(rb.e_s.cpu().numpy(), st.e_s))
         if ties or not exact:
             self.resync()
 

@@ -13,7 +13,7 @@ pytestmark = pytest.mark.gpu
 if not torch.cuda.is_available():  # pragma: no cover - CPU-only host
     pytest.skip("needs a GPU", allow_module_level=True)
 
-from parity_util import Pair, qfields  # noqa: E402
+from parity_util import Pair, qfields, same_values  # noqa: E402
 
 SIGN = lambda b, ef=1: qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, ef, b)  # noqa: E731
 STOCH = lambda bits, sc, b, ef=1: qfields(O.Q_STOCH_UNIFORM, bits, sc, ef, b)  # noqa: E731
@@ -166,6 +166,46 @@ def test_many_workers(N):
     _run(d, N, STOCH(4, O.SCALE_L2, 512), STOCH(4, O.SCALE_L2, 512), O.ADAM_AT_SERVER, T=2)
     _run(d, N, STOCH(4, O.SCALE_MAX, 512), SIGN(256), O.ADAM_AT_WORKER, T=2)
     _run(d, N, qfields(O.Q_DET_UNIFORM, 2, bucket=512), SIGN(1024), O.ADAM_AT_SERVER, T=2)
+
+
+EXTREME_KINDS = {
+    "stoch4_l2": STOCH(4, O.SCALE_L2, 512),
+    "stoch2_max": STOCH(2, O.SCALE_MAX, 512),
+    "sign": SIGN(512),
+    "ex1": qfields(O.Q_DET_UNIFORM, 3, bucket=512),
+    "ex2": qfields(O.Q_POW2, kmin=-126, kmax=127),
+    "topk": qfields(O.Q_TOPK, bucket=512, keep=16),
+}
+
+
+@pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
+@pytest.mark.parametrize("kind", list(EXTREME_KINDS))
+def test_extreme_magnitudes(kind, placement):
+    """Buckets of subnormal gradients, of gradients near the binary32 maximum
+    (their squares, L2 norms and Adam second moments overflow to infinity), of
+    zeros, and mixed: both sides follow the same IEEE binary32 steps, so every
+    output still matches."""
+    import numpy as np
+    d, N = 512 * 6 + 64, 4
+    q = EXTREME_KINDS[kind]
+    pair = Pair(d, N, q, q, placement, seed=8, eps=0.0)
+    rng = np.random.default_rng(4)
+    for t in range(1, 4):
+        g = np.zeros((N, d), np.float32)
+        sgn = rng.choice(np.array([-1.0, 1.0], np.float32), size=(N, d))
+        g[:, 0:512] = sgn[:, 0:512] * rng.uniform(1, 100, (N, 512)).astype(np.float32) * np.float32(1e-43)
+        g[:, 512:1024] = sgn[:, 512:1024] * rng.uniform(0.5, 3.0, (N, 512)).astype(np.float32) * np.float32(1e38)
+        g[:, 1536:2048] = sgn[:, 1536:2048] * np.float32(1e30)
+        g[:, 2048:] = (sgn[:, 2048:] * rng.standard_normal((N, d - 2048)).astype(np.float32)
+                       * np.exp(rng.uniform(-80, 80, (N, d - 2048))).astype(np.float32))
+        pair.step(t, g)
+        # the float comparison cannot see NaN or infinite entries: require the
+        # state bit for bit, NaN in the same places
+        for name in ("x", "e_w", "e_s") + (("m", "v") if placement == O.ADAM_AT_SERVER else ("m_w", "v_w")):
+            got = getattr(pair.rb, name).cpu().numpy()
+            assert same_values(got, getattr(pair.ost, name)), f"step {t}: {name} differs"
+        assert pair.stats.resyncs == 0
+    pair.check_tie_budget()
 
 
 def test_zero_buckets_in_lean_kernels():
