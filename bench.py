@@ -57,6 +57,18 @@ def algorithmic_bytes(E, cfg) -> int:
     return N * (worker + 8 * ww + 4 * nw) + server + 8 * sw + 4 * ns
 
 
+def split_bytes(E, cfg) -> int:
+    """Minimum HBM bytes of the round made of the four split calls: the fused
+    round's, plus what the calls hand over through HBM: the worker messages
+    read back by ea_server_aggregate_adam, its output u written and read back
+    by ea_server_compress, and the server message read back by
+    ea_worker_apply."""
+    d, N = cfg.d, cfg.N
+    ww, sw = E.ea_msg_words(cfg.qw, d), E.ea_msg_words(cfg.qs, d)
+    nw, ns = E.ea_msg_scales(cfg.qw, d), E.ea_msg_scales(cfg.qs, d)
+    return algorithmic_bytes(E, cfg) + N * (8 * ww + 4 * nw) + 8 * d + 8 * sw + 4 * ns
+
+
 def traffic_from_profile(workload: str, placement: str):
     """HBM bytes per round measured by rocprofv3 counters (FETCH_SIZE and
     WRITE_SIZE summed over the round's step_kernel launches, each scaled by
@@ -183,10 +195,11 @@ def main():
     ap.add_argument("--workload", default="bert", choices=list(W.WORKLOADS) + ["paper_toy"],
                     help="paper_toy: Section V-A's problem (d = 500, N = 10, Example 2, Adam at the "
                          "workers), each step = ea_toy_grad at the current x + one round")
-    ap.add_argument("--call", default="step", choices=["step", "scheduled", "graph"],
+    ap.add_argument("--call", default="step", choices=["step", "scheduled", "graph", "split"],
                     help="time ea_step (default), ea_step_scheduled with the step on the device and a "
-                         "Section V-B step-decay schedule, or that call captured once in a HIP graph and "
-                         "replayed")
+                         "Section V-B step-decay schedule, that call captured once in a HIP graph and "
+                         "replayed, or the four split calls (ea_worker_compress for each worker, "
+                         "ea_server_aggregate_adam, ea_server_compress, ea_worker_apply)")
     ap.add_argument("--placement", default="server", choices=["server", "worker"])
     ap.add_argument("--cpu-sample", type=int, default=1 << 24, help="parameters in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -224,7 +237,7 @@ def main():
     w = W.WORKLOADS[args.workload]
     placement = E.EA_ADAM_AT_SERVER if args.placement == "server" else E.EA_ADAM_AT_WORKER
     cfg = E.Config(**w.config_fields(placement=placement), qw=E.Quant(**w.qw.fields()), qs=E.Quant(**w.qs.fields()))
-    rb = allocate(cfg)
+    rb = allocate(cfg, with_u=args.call == "split")
     init_state(cfg, rb)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(w.seed)
@@ -246,10 +259,22 @@ def main():
         stream = torch.cuda.current_stream()
     t = 1
 
+    nsw, nss = E.ea_msg_scales(cfg.qw, cfg.d), E.ea_msg_scales(cfg.qs, cfg.d)
+
     def one_round():
         nonlocal t
         if args.call == "step":
             E.ea_step(cfg, t, **rb.step_args(), stream=stream)
+        elif args.call == "split":
+            for i in range(cfg.N):
+                E.ea_worker_compress(cfg, i, t, rb.g[i], rb.e_w[i], None if rb.m_w is None else rb.m_w[i],
+                                     None if rb.v_w is None else rb.v_w[i], rb.wcodes[i],
+                                     rb.wscales[i] if nsw else None, rb.workspace, stream=stream)
+            E.ea_server_aggregate_adam(cfg, t, rb.wcodes, rb.wscales if nsw else None, rb.m, rb.v, rb.u,
+                                       stream=stream)
+            E.ea_server_compress(cfg, t, rb.u, rb.e_s, rb.scodes, rb.sscales if nss else None, rb.workspace,
+                                 stream=stream)
+            E.ea_worker_apply(cfg, rb.scodes, rb.sscales if nss else None, rb.x, stream=stream)
         elif args.call == "scheduled":
             E.ea_step_scheduled(cfg, sched, t_dev, **rb.step_args(), stream=stream)
         else:
@@ -267,12 +292,15 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
 
-    alg = algorithmic_bytes(E, cfg)
+    alg = split_bytes(E, cfg) if args.call == "split" else algorithmic_bytes(E, cfg)
     achieved = alg / (ms * 1e-3) / 1e9
     value = cfg.d / (ms * 1e-3) / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(args.workload, args.placement),
-            "kernel": "step_kernel (whole tiles + ragged tail)", "algorithmic_bytes_per_round": alg,
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": None if args.call == "split" else traffic_from_profile(args.workload, args.placement),
+            "kernel": ("worker_kernel x N, aggregate_kernel, server_kernel, apply_kernel" if args.call == "split"
+                       else "step_kernel (whole tiles + ragged tail)"),
+            "algorithmic_bytes_per_round": alg,
             "bytes_per_param": round(alg / cfg.d, 2)}
     line = {
         "metric": METRIC, "value": round(value, 4), "unit": "Gparam/s", "n_gpus": 1, "steps": args.steps,

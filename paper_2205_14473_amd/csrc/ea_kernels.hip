@@ -115,16 +115,39 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
     if (!tile_pos<C>(a, t)) return;
     const int lane = lane_id();
     float4 acc[C], dq[C], u[C];
+    ServerRows<C> sr;
+    load_server<C, VEC, false, -1>(a, t.base, t.nch, false, false, sr);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
+    // Bit-plane messages: the next worker's code words and scales are loaded
+    // while the current worker's are decoded.
+    const bool planes = plane_coded<QRt>(a.qw);
+    uint64_t wv[C];
+    float sc[C];
+    if (planes) {
+        load_code_words<C, QRt>(a.qw, a.wcodes, t.base, t.nch, wv);
+        load_chunk_scales<C, QRt>(a.qw, a.wscales, t.base, t.nch, sc);
+    }
     for (int i = 0; i < a.N; ++i) {
-        dequant_tile<C, QRt>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales,
-                             t.base, t.nch, a.d, dq);
+        if (planes) {
+            const int64_t j = i + 1 < a.N ? i + 1 : i;
+            uint64_t nwv[C];
+            float nsc[C];
+            load_code_words<C, QRt>(a.qw, a.wcodes + j * a.qw.words, t.base, t.nch, nwv);
+            load_chunk_scales<C, QRt>(a.qw, a.wscales + j * a.qw.nscales, t.base, t.nch, nsc);
+            decode_words<C, QRt>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, dq);
+#pragma unroll
+            for (int ch = 0; ch < C; ++ch) {
+                wv[ch] = nwv[ch];
+                sc[ch] = nsc[ch];
+            }
+        } else {
+            dequant_tile<C, QRt>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
+                                 a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, dq);
+        }
 #pragma unroll
         for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
     }
-    ServerRows<C> sr;
-    load_server<C, VEC, false, -1>(a, t.base, t.nch, false, false, sr);
     server_input<C, VEC, false, -1>(a, acc, t.base, t.nch, sr, u);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch)

@@ -560,6 +560,78 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
     }
 }
 
+// A bit-plane message's code words for one tile, one word per lane: lane j
+// holds word j of chunk ch (j < 4*bits <= 36).  One coalesced load per chunk
+// replaces a uniform load per slot and plane, so a worker's words can be in
+// flight while the previous worker's are decoded.
+template <int C, class QT>
+__device__ __forceinline__ void load_code_words(const QDev& q, const uint64_t* __restrict__ codes, int64_t base,
+                                                int nch, uint64_t (&wv)[C])
+{
+    const int lane = lane_id();
+    const int nw = 4 * QT::bits(q);
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        wv[ch] = 0u;
+        if (ch < nch && lane < nw) wv[ch] = codes[((base >> 8) + ch) * nw + lane];
+    }
+}
+
+// The scale of each chunk's bucket (1 for kinds without scales).
+template <int C, class QT>
+__device__ __forceinline__ void load_chunk_scales(const QDev& q, const float* __restrict__ scales, int64_t base,
+                                                  int nch, float (&sc)[C])
+{
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        sc[ch] = 1.0f;
+        const int64_t chunk = (base >> 8) + ch;
+        if (has_scale<QT>(q) && ch < nch) sc[ch] = scales[QT::cpb(q) == 0 ? 0 : (chunk >> QT::cpb_shift(q))];
+    }
+}
+
+// Decode one tile from its code words (load_code_words) and chunk scales:
+// bit p of the code of slot k is bit `lane` of word k*bits + p, read from the
+// lane that holds it.
+template <int C, class QT>
+__device__ __forceinline__ void decode_words(const QDev& q, const float* lut, const uint64_t (&wv)[C],
+                                             const float (&scs)[C], int64_t base, int nch, int64_t d,
+                                             float4 (&deq)[C])
+{
+    const int lane = lane_id();
+    const int bits = QT::bits(q);
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        deq[ch] = zero4();
+        if (ch >= nch) continue;
+        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
+        const float sc = uniform(scs[ch]);
+        const bool ok = !scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc));
+        const uint32_t lo = (uint32_t)wv[ch], hi = (uint32_t)(wv[ch] >> 32);
+        const int nv = nvalid4(n, d);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            uint32_t cc = 0;
+            for (int pl = 0; pl < bits; ++pl) {
+                const int j = k * bits + pl;
+                const uint32_t wl = (uint32_t)__builtin_amdgcn_readlane((int)lo, j);
+                const uint32_t wh = (uint32_t)__builtin_amdgcn_readlane((int)hi, j);
+                cc |= (((lane < 32 ? wl : wh) >> (lane & 31)) & 1u) << pl;
+            }
+            const float dv = ok ? deq_of<QT>(q, lut, cc, 0.0f, sc) : 0.0f;
+            set_comp(deq[ch], k, k < nv ? dv : 0.0f);
+        }
+    }
+}
+
+// Whether a message is bit planes (decoded with load_code_words and
+// decode_words) rather than raw values or a sparsifier's mask and values.
+template <class QT>
+__device__ __forceinline__ bool plane_coded(const QDev& q)
+{
+    return !is_sparse<QT>(q) && QT::kind(q) != Q_NONE;
+}
+
 // Dequantize one tile of a message (the inverse of the code table).
 template <int C, class QT>
 __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, const uint64_t* __restrict__ codes,
@@ -567,7 +639,6 @@ __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, co
                                              float4 (&deq)[C])
 {
     const int lane = lane_id();
-    const int bits = QT::bits(q);
     if (is_sparse<QT>(q)) {
         // Kept elements take their bucket's values in element order; the
         // count of kept elements before a chunk restarts at each bucket.
@@ -602,29 +673,18 @@ __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, co
         }
         return;
     }
+    if (plane_coded<QT>(q)) {
+        uint64_t wv[C];
+        float sc[C];
+        load_code_words<C, QT>(q, codes, base, nch, wv);
+        load_chunk_scales<C, QT>(q, scales, base, nch, sc);
+        decode_words<C, QT>(q, lut, wv, sc, base, nch, d, deq);
+        return;
+    }
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        deq[ch] = zero4();
-        if (ch >= nch) continue;
-        if (QT::kind(q) == Q_NONE) {
-            deq[ch] = ld4<false>(reinterpret_cast<const float*>(codes), n, d);
-            continue;
-        }
-        const int64_t chunk = (base >> 8) + ch;
-        float sc = 1.0f;
-        if (has_scale<QT>(q)) sc = scales[QT::cpb(q) == 0 ? 0 : (chunk >> QT::cpb_shift(q))];
-        sc = uniform(sc);
-        const bool ok = !scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc));
-        const uint64_t* w = codes + chunk * 4 * bits;
-        const int nv = nvalid4(n, d);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            uint32_t cc = 0;
-            for (int pl = 0; pl < bits; ++pl) cc |= (uint32_t)((w[k * bits + pl] >> lane) & 1u) << pl;
-            const float dv = ok ? deq_of<QT>(q, lut, cc, 0.0f, sc) : 0.0f;
-            set_comp(deq[ch], k, k < nv ? dv : 0.0f);
-        }
+        deq[ch] = ch < nch ? ld4<false>(reinterpret_cast<const float*>(codes), n, d) : zero4();
     }
 }
 
