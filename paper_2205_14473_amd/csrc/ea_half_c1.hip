@@ -1,4 +1,4 @@
-// ea_half_c1.hip -- fused-round kernels for buckets of 256 elements
+// ea_half_c1.hip -- fused-round and split-call kernels for buckets of 256 elements
 // (1 chunk per tile) with the worker quantizer fixed at compile time: scaled
 // sign, stochastic uniform with 1, 2, 4 or 8 bits and an L2 or max-norm
 // scale, top-k and random-k.  The server quantizer and the Adam placement are
@@ -14,7 +14,8 @@ template <class QW>
 constexpr HalfKernel half()
 {
     return HalfKernel{1, QW::kind(QDev{}), QW::bits(QDev{}), QW::norm(QDev{}), QW::cpb(QDev{}),
-                      step_kernel<1, true, true, QW, QRt, -1>, kernel_tiles(1, true, -1, true)};
+                      step_kernel<1, true, true, QW, QRt, -1>, kernel_tiles(1, true, -1, true),
+                      worker_kernel<1, true, QW>, aggregate_kernel<1, true, QW>};
 }
 
 const HalfKernel kHalf[] = {

@@ -73,87 +73,6 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(const double* __restri
     }
 }
 
-// Split call: worker a.worker compresses its row (a.g, a.e_w, a.m_w, a.v_w
-// point at that worker's d-vectors; a.wcodes/a.wscales at its message).
-template <int C, bool VEC>
-__global__ __launch_bounds__(kBlock) void worker_kernel(StepArgs a)
-{
-    __shared__ float lut_w[kLutSize];
-    fill_lut(a.qw, lut_w);
-    __syncthreads();
-    TilePos t;
-    if (!tile_pos<C>(a, t)) return;
-    const int lane = lane_id();
-    const bool wglobal = has_scale<QRt>(a.qw) && a.qw.cpb == 0;
-    const bool atw = a.placement == AT_WORKER;
-    WorkerRows<C> r;
-    float4 p[C], dq[C];
-    load_worker<C, VEC, false, -1>(a, a.g, a.e_w, a.m_w, a.v_w, t.base, t.nch, r);
-    worker_p<C, -1>(a, r, p);
-    if (atw) store_moments<C, VEC, false, -1>(a, a.m_w, a.v_w, t.base, t.nch, r);
-    const float gs = wglobal ? a.wscales[0] : 0.0f;
-    WordSink sink = message_sink<QRt>(a.qw, a.wcodes, t.base);
-    quantize_tile<C, false, QRt>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)a.worker, gs,
-                                 a.wcodes, a.wscales, sink, dq);
-    sink.flush();
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (ch >= t.nch) continue;
-        st4<VEC>(a.e_w, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, a.qw.ef ? sub4(p[ch], dq[ch]) : zero4());
-    }
-}
-
-// Split call: dequantize the N worker messages, average in ascending worker
-// order, run Adam at the server if placed there; result in a.ubuf.
-template <int C, bool VEC>
-__global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
-{
-    __shared__ float lut_w[kLutSize];
-    fill_lut(a.qw, lut_w);
-    __syncthreads();
-    TilePos t;
-    if (!tile_pos<C>(a, t)) return;
-    const int lane = lane_id();
-    float4 acc[C], dq[C], u[C];
-    ServerRows<C> sr;
-    load_server<C, VEC, false, -1>(a, t.base, t.nch, false, false, sr);
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
-    // Bit-plane messages: the next worker's code words and scales are loaded
-    // while the current worker's are decoded.
-    const bool planes = plane_coded<QRt>(a.qw);
-    uint64_t wv[C];
-    float sc[C];
-    if (planes) {
-        load_code_words<C, QRt>(a.qw, a.wcodes, t.base, t.nch, wv);
-        load_chunk_scales<C, QRt>(a.qw, a.wscales, t.base, t.nch, sc);
-    }
-    for (int i = 0; i < a.N; ++i) {
-        if (planes) {
-            const int64_t j = i + 1 < a.N ? i + 1 : i;
-            uint64_t nwv[C];
-            float nsc[C];
-            load_code_words<C, QRt>(a.qw, a.wcodes + j * a.qw.words, t.base, t.nch, nwv);
-            load_chunk_scales<C, QRt>(a.qw, a.wscales + j * a.qw.nscales, t.base, t.nch, nsc);
-            decode_words<C, QRt>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, dq);
-#pragma unroll
-            for (int ch = 0; ch < C; ++ch) {
-                wv[ch] = nwv[ch];
-                sc[ch] = nsc[ch];
-            }
-        } else {
-            dequant_tile<C, QRt>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
-                                 a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, dq);
-        }
-#pragma unroll
-        for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
-    }
-    server_input<C, VEC, false, -1>(a, acc, t.base, t.nch, sr, u);
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch)
-        if (ch < t.nch) st4<VEC>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
-}
-
 // Server compression from u (a.ubuf) and e_s; optionally also x -= message.
 template <int C, bool VEC>
 __global__ __launch_bounds__(kBlock) void server_kernel(StepArgs args)
@@ -388,14 +307,26 @@ hipError_t launch_finalize(const double* part, int64_t ntiles, int32_t norm, int
     return hipGetLastError();
 }
 
+// The split calls on the worker side use a kernel specialized for the worker
+// quantizer when one matches and rows are aligned, else the generic one.
 hipError_t launch_worker(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
+    const HalfKernel* hk = vec ? find_half(a, C) : nullptr;
+    if (hk) {
+        hipLaunchKernelGGL(hk->worker, dim3((unsigned)grid_of(a)), dim3(kBlock), 0, s, a);
+        return hipGetLastError();
+    }
     EA_DISPATCH(worker_kernel, C, vec, grid_of(a), s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_aggregate(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
+    const HalfKernel* hk = vec ? find_half(a, C) : nullptr;
+    if (hk) {
+        hipLaunchKernelGGL(hk->aggregate, dim3((unsigned)grid_of(a)), dim3(kBlock), 0, s, a);
+        return hipGetLastError();
+    }
     EA_DISPATCH(aggregate_kernel, C, vec, grid_of(a), s, a);
     return hipGetLastError();
 }

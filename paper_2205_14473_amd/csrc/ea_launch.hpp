@@ -53,14 +53,17 @@ struct StepArgs {
 // Launchers; C = chunks per tile (1..8), vec = rows are 16-byte aligned.
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s);
 
-// Fused-round kernels specialized for the worker quantizer only (kind, code
-// bits, norm and chunks per bucket fixed; the server quantizer and the Adam
-// placement read at run time), for whole tiles of C = chunks-per-bucket
-// chunks.  One table per C, each compiled in its own translation unit.
+// Kernels specialized for the worker quantizer only (kind, code bits, norm
+// and chunks per bucket fixed; the server quantizer and the Adam placement
+// read at run time): the fused round for whole tiles of C = chunks-per-bucket
+// chunks, and the split calls on the worker side.  One table per C, each
+// compiled in its own translation unit.
 struct HalfKernel {
     int C, wkind, wbits, wnorm, wcpb;
     void (*kernel)(StepArgs);
     int tiles;                // tiles per block
+    void (*worker)(StepArgs);     // split call: one worker's compression (aligned rows)
+    void (*aggregate)(StepArgs);  // split call: decode and average of the N messages
 };
 const HalfKernel* half_kernels_c1(int* n);
 const HalfKernel* half_kernels_c2(int* n);

@@ -1019,6 +1019,90 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
 // Kernels
 // ---------------------------------------------------------------------------
 
+// Split call: worker a.worker compresses its row (a.g, a.e_w, a.m_w, a.v_w
+// point at that worker's d-vectors; a.wcodes/a.wscales at its message).
+// Blocks of 4 independent waves, one tile each; QW fixes the worker
+// quantizer at compile time (by default it is read at run time).
+template <int C, bool VEC, class QW = QRt>
+__global__ __launch_bounds__(kBlock) void worker_kernel(StepArgs a)
+{
+    __shared__ float lut_w[kLutSize];
+    fill_lut(a.qw, lut_w);
+    __syncthreads();
+    TilePos t;
+    if (!tile_pos<C>(a, t)) return;
+    const int lane = lane_id();
+    const bool wglobal = has_scale<QW>(a.qw) && QW::cpb(a.qw) == 0;
+    const bool atw = a.placement == AT_WORKER;
+    WorkerRows<C> r;
+    float4 p[C], dq[C];
+    load_worker<C, VEC, false, -1>(a, a.g, a.e_w, a.m_w, a.v_w, t.base, t.nch, r);
+    worker_p<C, -1>(a, r, p);
+    if (atw) store_moments<C, VEC, false, -1>(a, a.m_w, a.v_w, t.base, t.nch, r);
+    const float gs = wglobal ? a.wscales[0] : 0.0f;
+    WordSink sink = message_sink<QW>(a.qw, a.wcodes, t.base);
+    quantize_tile<C, false, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)a.worker, gs,
+                                 a.wcodes, a.wscales, sink, dq);
+    sink.flush();
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        if (ch >= t.nch) continue;
+        st4<VEC>(a.e_w, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, a.qw.ef ? sub4(p[ch], dq[ch]) : zero4());
+    }
+}
+
+// Split call: dequantize the N worker messages, average in ascending worker
+// order, run Adam at the server if placed there; result in a.ubuf.
+template <int C, bool VEC, class QW = QRt>
+__global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
+{
+    __shared__ float lut_w[kLutSize];
+    fill_lut(a.qw, lut_w);
+    __syncthreads();
+    TilePos t;
+    if (!tile_pos<C>(a, t)) return;
+    const int lane = lane_id();
+    float4 acc[C], dq[C], u[C];
+    ServerRows<C> sr;
+    load_server<C, VEC, false, -1>(a, t.base, t.nch, false, false, sr);
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
+    // Bit-plane messages: the next worker's code words and scales are loaded
+    // while the current worker's are decoded.
+    const bool planes = plane_coded<QW>(a.qw);
+    uint64_t wv[C];
+    float sc[C];
+    if (planes) {
+        load_code_words<C, QW>(a.qw, a.wcodes, t.base, t.nch, wv);
+        load_chunk_scales<C, QW>(a.qw, a.wscales, t.base, t.nch, sc);
+    }
+    for (int i = 0; i < a.N; ++i) {
+        if (planes) {
+            const int64_t j = i + 1 < a.N ? i + 1 : i;
+            uint64_t nwv[C];
+            float nsc[C];
+            load_code_words<C, QW>(a.qw, a.wcodes + j * a.qw.words, t.base, t.nch, nwv);
+            load_chunk_scales<C, QW>(a.qw, a.wscales + j * a.qw.nscales, t.base, t.nch, nsc);
+            decode_words<C, QW>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, dq);
+#pragma unroll
+            for (int ch = 0; ch < C; ++ch) {
+                wv[ch] = nwv[ch];
+                sc[ch] = nsc[ch];
+            }
+        } else {
+            dequant_tile<C, QW>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
+                                 a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, dq);
+        }
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
+    }
+    server_input<C, VEC, false, -1>(a, acc, t.base, t.nch, sr, u);
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch)
+        if (ch < t.nch) st4<VEC>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
+}
+
+
 // Floats of the code-table region of a fused-round block with G waves: room
 // for both block-wide tables or for two 64-entry tables per wave.
 __host__ __device__ constexpr int table_floats(int G)
