@@ -353,7 +353,10 @@ int step_impl(const char* name, const ea_config_t* c, int64_t t, uint32_t* t_dev
         a.spart = (double*)((char*)workspace + p.off_spart);
         a.ubuf = (float*)((char*)workspace + p.off_ubuf);
     }
-    const bool vec = vec_ok(c->d, {g, e_w, a.m_w, a.v_w, a.m, a.v, e_s, x, a.ubuf});
+    // Messages sent as raw values are written as float4 by whole-tile kernels.
+    const bool vec = vec_ok(c->d, {g, e_w, a.m_w, a.v_w, a.m, a.v, e_s, x, a.ubuf,
+                                   c->qw.kind == EA_Q_NONE ? (const void*)wcodes : nullptr,
+                                   c->qs.kind == EA_Q_NONE ? (const void*)scodes : nullptr});
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = hipSuccess;
     if (p.wglobal) {

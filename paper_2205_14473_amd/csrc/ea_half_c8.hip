@@ -1,9 +1,11 @@
 // ea_half_c8.hip -- fused-round and split-call kernels for buckets of 2048 elements
 // (8 chunks per tile) with the worker quantizer fixed at compile time: scaled
 // sign, stochastic uniform with 1, 2, 4 or 8 bits and an L2 or max-norm
-// scale, top-k and random-k.  The server quantizer and the Adam placement are
-// read at run time.  The workers' per-element work is N times the server's,
-// so these kernels run close to the fully specialized ones.
+// scale, top-k, random-k, Example 1 with 2 or 3 bits, and (with no bucket,
+// so at any tile size) Example 2 with 4-bit codes and full precision.  The
+// server quantizer and the Adam placement are read at run time.  The
+// workers' per-element work is N times the server's, so these kernels run
+// close to the fully specialized ones.
 #include "ea_round.hpp"
 
 namespace ea {
@@ -30,6 +32,10 @@ const HalfKernel kHalf[] = {
     half<QCt<Q_STOCH, 8, S_MAX, 8>>(),
     half<QCt<Q_TOPK, 1, S_MAX, 8>>(),
     half<QCt<Q_RANDK, 1, S_MAX, 8>>(),
+    half<QCt<Q_DET, 2, S_MAX, 8>>(),
+    half<QCt<Q_DET, 3, S_MAX, 8>>(),
+    half<QCt<Q_POW2, 4, S_MAX, 0>>(),
+    half<QCt<Q_NONE, 32, S_MAX, 0>>(),
 };
 
 }  // namespace

@@ -213,10 +213,12 @@ const Special* find_special(const StepArgs& a, int C)
 }
 
 // A kernel specialized for the worker quantizer, when one matches: whole
-// tiles of one worker bucket each.
+// tiles of one worker bucket each, or of any size for a worker quantizer
+// without buckets (Example 2, full precision).
 const HalfKernel* find_half(const StepArgs& a, int C)
 {
-    if (a.qw.cpb != C) return nullptr;
+    const bool bucketless = a.qw.kind == Q_POW2 || a.qw.kind == Q_NONE;
+    if (a.qw.cpb != (bucketless ? 0 : C)) return nullptr;
     int n = 0;
     const HalfKernel* t = C == 1 ? half_kernels_c1(&n) : C == 2 ? half_kernels_c2(&n)
                         : C == 4 ? half_kernels_c4(&n) : C == 8 ? half_kernels_c8(&n) : nullptr;

@@ -490,11 +490,15 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
 
     const bool gated = scale_gated<QT>(q);
     if (kind == Q_NONE) {
+        // Whole tiles: the raw message is 16-byte aligned (the launcher
+        // requires it of messages sent as values before it takes them).
         float* raw = reinterpret_cast<float*>(codes);
 #pragma unroll
         for (int ch = 0; ch < C; ++ch) {
             deq[ch] = p[ch];
-            if (FULL || ch < nch) st4<false>(raw, base + (int64_t)ch * kChunk + 4 * lane, d, p[ch]);
+            const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
+            if (FULL) st4<true, true>(raw, n, d, p[ch]);
+            else if (ch < nch) st4<false>(raw, n, d, p[ch]);
         }
         return;
     }

@@ -1,11 +1,12 @@
 """GPU parity of the fused-round kernels specialized for the worker quantizer
 only (the server quantizer and the Adam placement read at run time): every
 worker quantizer of those tables (scaled sign; stochastic 1/2/4/8-bit with L2
-or max-norm scale; top-k; random-k) at every bucket size 256 to 2048, paired
-with a different server quantizer whose bucket is no larger, in both
-placements.  Sizes hold several whole tiles (the specialized launch) and a
-ragged tail (the generic edge launch); one-chunk tiles go two to a block, so
-odd and even tile counts both occur."""
+or max-norm scale; top-k; random-k; Example 1 with 2 or 3 bits) at every
+bucket size 256 to 2048, paired with a different server quantizer whose bucket
+is no larger, in both placements; Example 2 and full precision (no bucket) at
+the tile size of the server's bucket.  Sizes hold several whole tiles (the
+specialized launch) and a ragged tail (the generic edge launch); one-chunk
+tiles go two to a block, so odd and even tile counts both occur."""
 import pytest
 
 import oracle as O
@@ -31,6 +32,11 @@ WORKER = {
     "stoch8_max": lambda b: qfields(O.Q_STOCH_UNIFORM, 8, O.SCALE_MAX, 1, b),
     "topk": lambda b: qfields(O.Q_TOPK, bucket=b, keep=b // 32 + 1),
     "randk": lambda b: qfields(O.Q_RANDK, bucket=b, keep=b // 16),
+    "ex1_2": lambda b: qfields(O.Q_DET_UNIFORM, 2, bucket=b),
+    "ex1_3": lambda b: qfields(O.Q_DET_UNIFORM, 3, bucket=b),
+    # no bucket: the tile size follows the server's bucket
+    "ex2_4": lambda b: qfields(O.Q_POW2, kmin=-17, kmax=-11),
+    "none": lambda b: qfields(O.Q_NONE),
 }
 # A server quantizer of another kind, bucket no larger than the worker's.
 SERVER = [
@@ -52,6 +58,8 @@ def test_worker_specialized_kernels(kind, bucket):
     qw = WORKER[kind](bucket)
     k = list(WORKER).index(kind)
     qs = SERVER[k % len(SERVER)](bucket)
+    if kind in ("ex2_4", "none"):      # the server's bucket sets the tile size
+        qs = qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, 1, bucket)
     placement = O.ADAM_AT_SERVER if k % 2 == 0 else O.ADAM_AT_WORKER
     tiles = 5 if bucket > 256 else 6          # one-chunk tiles: an even count, plus the tail
     d = bucket * tiles + 100

@@ -208,6 +208,24 @@ def test_extreme_magnitudes(kind, placement):
     pair.check_tie_budget()
 
 
+def test_full_precision_messages_unaligned():
+    """Messages sent as raw values go out as float4 only when the message
+    buffers are 16-byte aligned: an 8-byte aligned worker message array takes
+    the checked kernels and gives the same results."""
+    d, N = 512 * 6 + 64, 4
+    q = qfields(O.Q_NONE)
+    for shift in (0, 1):
+        pair = Pair(d, N, q, STOCH(2, O.SCALE_MAX, 512), O.ADAM_AT_SERVER, seed=6)
+        if shift:
+            words = pair.rb.wcodes.shape[1]
+            big = torch.zeros(N * words + 1, dtype=torch.uint64, device="cuda")
+            pair.rb.wcodes = big[1:].view(N, words)
+            assert pair.rb.wcodes.data_ptr() % 16 == 8
+        for t in range(1, 4):
+            pair.step(t, _grads("student_t", 6, t, N, d))
+        pair.check_tie_budget()
+
+
 def test_zero_buckets_in_lean_kernels():
     """Buckets whose scale is zero take the wave-uniform branch of the
     specialized kernels (bert quantizers, Adam at the server)."""
