@@ -31,7 +31,8 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "Efficient-Adam step throughput (Gparam/s, N workers) + % of HBM peak GB/s"
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2205_14473_amd", "csrc", f)
                   for f in ("ea_round.hpp", "ea_kernels.hip", "ea_half_c1.hip", "ea_half_c2.hip", "ea_half_c4.hip",
-                            "ea_half_c8.hip", "ea_device.hpp", "ea_launch.hpp", "ea_api.cpp")]
+                            "ea_half_c8.hip", "ea_sym_c4.hip", "ea_sym_c8.hip", "ea_device.hpp", "ea_launch.hpp",
+                            "ea_api.cpp")]
 
 
 def source_digest() -> str:

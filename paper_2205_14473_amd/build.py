@@ -14,7 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libea.so")
 SOURCES = [os.path.join(CSRC, f) for f in ("ea_kernels.hip", "ea_half_c1.hip", "ea_half_c2.hip", "ea_half_c4.hip",
-                                            "ea_half_c8.hip", "ea_toy.hip", "ea_api.cpp")]
+                                            "ea_half_c8.hip", "ea_sym_c4.hip", "ea_sym_c8.hip", "ea_toy.hip",
+                                            "ea_api.cpp")]
 HEADERS = [os.path.join(CSRC, f) for f in ("ea_device.hpp", "ea_launch.hpp", "ea_round.hpp")] + \
     [os.path.join(ROOT, "include", "ea.h")]
 ARCH = "gfx950"

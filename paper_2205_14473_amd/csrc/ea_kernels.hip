@@ -230,6 +230,21 @@ const HalfKernel* find_half(const StepArgs& a, int C)
     return nullptr;
 }
 
+// A fully specialized kernel for a wide tile with the same quantizer on both
+// sides and Adam at the server, when one matches.
+const SymKernel* find_sym(const StepArgs& a, int C)
+{
+    if (a.placement != AT_SERVER || (C != 4 && C != 8)) return nullptr;
+    const QDev& w = a.qw;
+    const QDev& v = a.qs;
+    if (w.kind != v.kind || w.bits != v.bits || w.norm != v.norm || w.cpb != v.cpb || w.cpb != C) return nullptr;
+    int n = 0;
+    const SymKernel* t = C == 4 ? sym_kernels_c4(&n) : sym_kernels_c8(&n);
+    for (int i = 0; i < n; ++i)
+        if (t[i].kind == w.kind && t[i].bits == w.bits && t[i].norm == w.norm && t[i].cpb == w.cpb) return &t[i];
+    return nullptr;
+}
+
 }  // namespace
 
 // Whole tiles go to a kernel without bounds checks: one specialized for both
@@ -242,9 +257,10 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
     const size_t limit = lds_limit_bytes();
     const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) : 0;
     const Special* sp = vec ? find_special(a, C) : nullptr;
-    const HalfKernel* hk = vec && !sp ? find_half(a, C) : nullptr;
+    const SymKernel* sk = vec && !sp ? find_sym(a, C) : nullptr;
+    const HalfKernel* hk = vec && !sp && !sk ? find_half(a, C) : nullptr;
     if (nfull > 0) {
-        const int K = sp ? sp->tiles : hk ? hk->tiles : round_tiles_per_block(C, false);
+        const int K = sp ? sp->tiles : sk ? sk->tiles : hk ? hk->tiles : round_tiles_per_block(C, false);
         const int G = round_waves(a.N, C, K, limit);
         StepArgs b = a;
         b.tile0 = 0;
@@ -253,6 +269,8 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
         const size_t lds = round_lds_bytes(a.N, C, G, K);
         if (sp) {
             hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
+        } else if (sk) {
+            hipLaunchKernelGGL(sk->kernel, grid, block, lds, s, b);
         } else if (hk) {
             hipLaunchKernelGGL(hk->kernel, grid, block, lds, s, b);
         } else {

@@ -65,6 +65,16 @@ struct HalfKernel {
     void (*worker)(StepArgs);     // split call: one worker's compression (aligned rows)
     void (*aggregate)(StepArgs);  // split call: decode and average of the N messages
 };
+// Fully specialized fused-round kernels for the same quantizer on both sides
+// with Adam at the server, for wide tiles (C = 4, 8), where a run-time server
+// quantizer costs most (its registers set the whole block's).
+struct SymKernel {
+    int C, kind, bits, norm, cpb;
+    void (*kernel)(StepArgs);
+    int tiles;
+};
+const SymKernel* sym_kernels_c4(int* n);
+const SymKernel* sym_kernels_c8(int* n);
 const HalfKernel* half_kernels_c1(int* n);
 const HalfKernel* half_kernels_c2(int* n);
 const HalfKernel* half_kernels_c4(int* n);

@@ -1150,12 +1150,16 @@ size_t lds_limit_bytes()
 // wscales (computed beforehand); with a one-bucket Q_s the block stops after
 // the server input, which it leaves in ubuf with per-tile partial norms.
 //
+// MW > 0 overrides the minimum waves per SIMD of the launch bounds (the
+// register cap).
+//
 // FULL kernels (rows 16-byte aligned) take the tiles that lie wholly inside d
 // and carry no bounds checks; the others take any tile.  A launch covers
 // tiles [a.tile0, a.tile1); block b works on the K tiles from
 // a.tile0 + b*K.
-template <int C, bool VEC, bool FULL, class QW, class QS, int PL>
-__global__ __launch_bounds__(max_round_waves(C) * kWave, round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
+template <int C, bool VEC, bool FULL, class QW, class QS, int PL, int MW = 0>
+__global__ __launch_bounds__(max_round_waves(C) * kWave,
+                             MW > 0 ? MW : round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
     StepArgs args)
 {
     const StepArgs a = with_step(args);

@@ -80,3 +80,19 @@ def test_worker_specialized_with_one_bucket_server(placement):
     for t in range(1, 4):
         pair.step(t, _grads(3, t, 6, d))
     pair.check_tie_budget()
+
+
+SYMMETRIC = ["sign", "stoch1_l2", "stoch2_max", "stoch4_l2", "stoch4_max", "stoch8_max", "topk", "randk"]
+
+
+@pytest.mark.parametrize("bucket", [1024, 2048])
+@pytest.mark.parametrize("kind", SYMMETRIC)
+def test_symmetric_wide_tiles(kind, bucket):
+    """The same quantizer on both sides with Adam at the server, 4- and 8-chunk
+    tiles: the fully specialized wide-tile kernels."""
+    q = WORKER[kind](bucket)
+    d = bucket * 5 + 100
+    pair = Pair(d, 6, q, q, O.ADAM_AT_SERVER, seed=21)
+    for t in range(1, 4):
+        pair.step(t, _grads(21, t, 6, d))
+    pair.check_tie_budget()
