@@ -151,11 +151,19 @@ __device__ __forceinline__ WordSink message_sink(const QDev& q, uint64_t* codes,
 }
 
 // Sparsifier tuning: how many of each lane's largest keys a first threshold
-// search runs on (0: none, 1 to 3), and whether the searches skip the bits
-// that all lane maxima share (1).
+// search runs on (0: none), for tiles of up to 2 chunks and for wider ones
+// (more keys per lane, so more of the kept ones can fall in one lane), and
+// whether the searches skip the bits that all lane maxima share (1).
 #ifndef EA_SPARSE_SUBSET
 #define EA_SPARSE_SUBSET 3
 #endif
+#ifndef EA_SPARSE_SUBSET_WIDE
+#define EA_SPARSE_SUBSET_WIDE 5
+#endif
+__host__ __device__ constexpr int sparse_subset(int C)
+{
+    return C >= 4 ? EA_SPARSE_SUBSET_WIDE : EA_SPARSE_SUBSET;
+}
 #ifndef EA_SPARSE_PREFIX
 #define EA_SPARSE_PREFIX 1
 #endif
@@ -192,11 +200,11 @@ __device__ __forceinline__ uint32_t wave_count(bool pred)
     return (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(pred));
 }
 
-// Bitwise OR and AND of a value over the wave (same steps as wave_max).
-__device__ __forceinline__ void wave_or_and(uint32_t v, uint32_t& o, uint32_t& a)
+// Bitwise OR over the wave of vo and AND of va (same steps as wave_max).
+__device__ __forceinline__ void wave_or_and(uint32_t vo, uint32_t va, uint32_t& o, uint32_t& a)
 {
-    o = v;
-    a = v;
+    o = vo;
+    a = va;
     o |= dpp<kDppXor1>(o);
     a &= dpp<kDppXor1>(a);
     o |= dpp<kDppXor2>(o);
@@ -223,15 +231,20 @@ __device__ __forceinline__ void wave_or_and(uint32_t v, uint32_t& o, uint32_t& a
 //
 // The k-th largest key T is found by a bitwise search (bit_select) that
 // counts with ballots; the search is the costly part, so three things cut its
-// steps and ballots.  (1) For k <= 64, T lies between the smallest and the
-// largest lane maximum, so the search starts below the bits all lane maxima
-// share (for magnitudes, typically the sign and most of the exponent).  (2) It first runs on each lane's three largest keys only (3
-// ballots a step instead of 4 per chunk) and keeps that answer when a full
-// count confirms it; else it runs again over every key.  (3) It stops as
-// soon as exactly k keys reach a candidate, which then splits the bucket
-// without ties.  Otherwise the keys equal to T are ranked by element index
-// (element n = 256c + 4l + s comes after every element of lower chunks, of
-// lower lanes of its chunk, and of lower slots of its lane).  The kept
+// steps and ballots.  (1) For k <= 64 r, T lies between the smallest of the
+// lanes' r-th largest keys and the largest key, so the search starts below
+// the bits those keys all share (for magnitudes, typically the sign and most
+// of the exponent); r runs up to S below.  (2)
+// For k <= 16 S it first runs on each lane's S largest keys only (S ballots a
+// step instead of 4 per chunk; S = 3 for tiles of up to 2 chunks, 5 for wider
+// ones) and keeps that answer when a full count confirms it; else it runs
+// again over every key.  A lane then holds k/64 <= S/4 of the k largest keys
+// on average, so few buckets have a lane with more than S of them; for larger
+// k most do, and the first search would mostly be wasted.  (3) It stops as soon as exactly k keys reach a candidate,
+// which then splits the bucket without ties.  Otherwise the keys equal to T
+// are ranked by element index (element n = 256c + 4l + s comes after every
+// element of lower chunks, of lower lanes of its chunk, and of lower slots of
+// its lane).  The kept
 // values are listed in element order at positions counted the same way.
 // Elements past d get key 0 and the highest indices, so they rank below
 // every element of the vector and are never kept.
@@ -287,27 +300,36 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
         };
         uint32_t T = 0u, gt = 0u;
         bool exact = false, found = false, have_gt = false;
-        // The lanes' largest keys m[0] (and next largest m[1], m[2]).
-        uint32_t m[3] = {0u, 0u, 0u};
+        // Each lane's S largest keys, m[0] the largest.
+        constexpr int S = sparse_subset(C);
+        uint32_t m[S > 0 ? S : 1];
+#pragma unroll
+        for (int r = 0; r < (S > 0 ? S : 1); ++r) m[r] = 0u;
 #pragma unroll
         for (int j = 0; j < C; ++j) {
             if (j < b0 || j >= b0 + cpb) continue;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const uint32_t x = key[j][k];
-                if (EA_SPARSE_SUBSET > 2) m[2] = max(m[2], min(m[1], x));
-                if (EA_SPARSE_SUBSET > 1) m[1] = max(m[1], min(m[0], x));
+#pragma unroll
+                for (int r = (S > 0 ? S : 1) - 1; r > 0; --r) m[r] = max(m[r], min(m[r - 1], x));
                 m[0] = max(m[0], x);
             }
         }
-        // With kk <= 64 the threshold lies between the smallest and largest
-        // lane maximum (64 keys reach the smallest), so it has the bits that
-        // every lane maximum shares above the highest bit where they differ.
+        // With kk <= 64 r (r <= S) the threshold lies between the smallest
+        // r-th largest key of a lane (64 r keys reach it) and the largest
+        // key, so it has the bits that all lanes' largest and r-th largest
+        // keys share above the highest bit where two of them differ.
         int hi = top;
         uint32_t prefix = 0u;
-        if (EA_SPARSE_PREFIX && kk <= (uint32_t)kWave) {
+        constexpr int R = S > 0 ? S : 1;
+        if (EA_SPARSE_PREFIX && kk <= (uint32_t)(R * kWave)) {
+            uint32_t mr = m[0];
+#pragma unroll
+            for (int r = 1; r < R; ++r)
+                if (kk > (uint32_t)(r * kWave)) mr = m[r];
             uint32_t o, n;
-            wave_or_and(m[0], o, n);
+            wave_or_and(m[0] | mr, m[0] & mr, o, n);
             o = (uint32_t)__builtin_amdgcn_readfirstlane((int)o);
             n = (uint32_t)__builtin_amdgcn_readfirstlane((int)n);
             // bits above h: all of them for h < 0, none for h >= 31
@@ -316,8 +338,8 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
             if (hi > top) hi = top;
             prefix = n & above(hi);
         }
-        if (EA_SPARSE_SUBSET > 0 && kk <= (uint32_t)(EA_SPARSE_SUBSET * kWave)) {
-            // First on the keys that are among their lane's EA_SPARSE_SUBSET
+        if (S > 0 && kk <= (uint32_t)(S * kWave / 4)) {
+            // First on the keys that are among their lane's S
             // largest.  Its answer Tr holds for the bucket when the counts
             // agree: every key above Tr is among them (Tr is then the kk-th
             // largest of all), or, when exactly kk of them reach Tr, exactly
@@ -325,7 +347,7 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
             const auto count_sub = [&](uint32_t c) {
                 uint32_t n = 0u;
 #pragma unroll
-                for (int r = 0; r < EA_SPARSE_SUBSET; ++r) n += wave_count(m[r] >= c);
+                for (int r = 0; r < S; ++r) n += wave_count(m[r] >= c);
                 return n;
             };
             bool er;

@@ -7,6 +7,7 @@ is no larger, in both placements; Example 2 and full precision (no bucket) at
 the tile size of the server's bucket.  Sizes hold several whole tiles (the
 specialized launch) and a ragged tail (the generic edge launch); one-chunk
 tiles go two to a block, so odd and even tile counts both occur."""
+import numpy as np
 import pytest
 
 import oracle as O
@@ -95,4 +96,32 @@ def test_symmetric_wide_tiles(kind, bucket):
     pair = Pair(d, 6, q, q, O.ADAM_AT_SERVER, seed=21)
     for t in range(1, 4):
         pair.step(t, _grads(21, t, 6, d))
+    pair.check_tie_budget()
+
+
+@pytest.mark.parametrize("bucket,keep", [(1024, 80), (1024, 81), (1024, 300), (2048, 1), (2048, 80), (2048, 81),
+                                         (2048, 700)])
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+def test_symmetric_wide_sparse_keeps(kind, bucket, keep):
+    """Wide-tile sparsifiers on both sides with keep on either side of the
+    limit below which the threshold search first runs on each lane's largest
+    keys, and far above it."""
+    q = qfields(O.Q_TOPK if kind == "topk" else O.Q_RANDK, bucket=bucket, keep=keep)
+    d = bucket * 4 + 300
+    pair = Pair(d, 4, q, q, O.ADAM_AT_SERVER, seed=keep)
+    for t in range(1, 4):
+        pair.step(t, _grads(keep, t, 4, d))
+    pair.check_tie_budget()
+
+
+@pytest.mark.parametrize("bucket", [1024, 2048])
+def test_symmetric_wide_topk_ties(bucket):
+    """Few distinct magnitudes: most keys tie at the threshold on wide tiles."""
+    d, N = bucket * 3 + 64, 3
+    q = qfields(O.Q_TOPK, bucket=bucket, keep=bucket // 32)
+    pair = Pair(d, N, q, q, O.ADAM_AT_SERVER, seed=8)
+    rng = np.random.default_rng(bucket)
+    for t in range(1, 4):
+        mag = rng.choice(np.array([0.0, 1e-3, 2e-3, 4e-3], np.float32), size=(N, d))
+        pair.step(t, (mag * rng.choice(np.array([-1.0, 1.0], np.float32), size=(N, d))).astype(np.float32))
     pair.check_tie_budget()

@@ -54,6 +54,16 @@ def test_lean_kernels(kind, d):
     _run(d, 16, q, q, O.ADAM_AT_SERVER, T=4)
 
 
+@pytest.mark.parametrize("gen", ["student_t", "tied"])
+@pytest.mark.parametrize("keep", [64, 65, 150, 192, 193])
+def test_lean_kernels_larger_keep(keep, gen):
+    """Bucket 512 with keep past one key per lane: the threshold search starts
+    below the bits shared by the lanes' largest and r-th largest keys for keep
+    up to 3 keys per lane (192), and from the top above that."""
+    q = TOPK(keep, 512)
+    _run(512 * 9 + 200, 6, q, q, O.ADAM_AT_SERVER, T=3, gen=gen, seed=keep)
+
+
 @pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
 @pytest.mark.parametrize("kind", list(SPARSE))
 @pytest.mark.parametrize("bucket,keep", [(256, 1), (512, 37), (1024, 200), (2048, 64)])
