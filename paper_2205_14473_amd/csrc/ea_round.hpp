@@ -586,20 +586,50 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
     }
 }
 
-// A bit-plane message's code words for one tile, one word per lane: lane j
-// holds word j of chunk ch (j < 4*bits <= 36).  One coalesced load per chunk
-// replaces a uniform load per slot and plane, so a worker's words can be in
-// flight while the previous worker's are decoded.
+// Widest code the traits allow (9 bits: Example 2 with the widest exponent
+// range).
+template <class QT>
+__host__ __device__ constexpr int max_code_bits()
+{
+    if constexpr (QT::fixed)
+        return QT::bits(QDev{});
+    else
+        return 9;
+}
+
+// A bit-plane message's code words for one tile, spread for decoding.  Bit
+// `lane` of a word lies in its low half for lanes 0-31 and in its high half
+// for lanes 32-63; of each chunk's 4*bits words, lane l holds that half of
+// word l mod 32 (x[ch][0]) and, for codes wider than 8 bits, of word
+// 32 + l mod 32 (x[ch][1]).  A decoding lane fetches the half it needs from
+// the lane that holds it (ds_bpermute).  Lanes past a chunk's words, and
+// chunks past the tile's end, load a word that exists and decode to nothing:
+// the loads take no branch, so the next worker's words stay in flight while
+// the current worker's are decoded.  (The select on the chunk count also
+// keeps the compiler from moving a prefetch's load into the next iteration,
+// where it would be waited for at once.)
+template <int C, class QT>
+struct CodeWords {
+    static constexpr int R = max_code_bits<QT>() > 8 ? 2 : 1;
+    uint32_t x[C][R];
+};
+
 template <int C, class QT>
 __device__ __forceinline__ void load_code_words(const QDev& q, const uint64_t* __restrict__ codes, int64_t base,
-                                                int nch, uint64_t (&wv)[C])
+                                                int nch, CodeWords<C, QT>& w)
 {
     const int lane = lane_id();
     const int nw = 4 * QT::bits(q);
+    const uint32_t* __restrict__ c32 = reinterpret_cast<const uint32_t*>(codes);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
-        wv[ch] = 0u;
-        if (ch < nch && lane < nw) wv[ch] = codes[((base >> 8) + ch) * nw + lane];
+        const int64_t chunk = (base >> 8) + (ch < nch ? ch : nch - 1);
+#pragma unroll
+        for (int r = 0; r < CodeWords<C, QT>::R; ++r) {
+            const int j = 32 * r + (lane & 31);
+            const uint32_t v = c32[(chunk * nw + (j < nw ? j : nw - 1)) * 2 + (lane >> 5)];
+            w.x[ch][r] = ch < nch ? v : 0u;
+        }
     }
 }
 
@@ -611,41 +641,44 @@ __device__ __forceinline__ void load_chunk_scales(const QDev& q, const float* __
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         sc[ch] = 1.0f;
-        const int64_t chunk = (base >> 8) + ch;
-        if (has_scale<QT>(q) && ch < nch) sc[ch] = scales[QT::cpb(q) == 0 ? 0 : (chunk >> QT::cpb_shift(q))];
+        if (has_scale<QT>(q)) {
+            const int64_t chunk = (base >> 8) + (ch < nch ? ch : nch - 1);
+            const float v = scales[QT::cpb(q) == 0 ? 0 : (chunk >> QT::cpb_shift(q))];
+            sc[ch] = ch < nch ? v : 1.0f;
+        }
     }
 }
 
-// Decode one tile from its code words (load_code_words) and chunk scales:
-// bit p of the code of slot k is bit `lane` of word k*bits + p, read from the
-// lane that holds it.
+// Decode one tile from its spread code words (load_code_words) and chunk
+// scales: bit p of the code of slot k is bit `lane` of word k*bits + p.
 template <int C, class QT>
-__device__ __forceinline__ void decode_words(const QDev& q, const float* lut, const uint64_t (&wv)[C],
+__device__ __forceinline__ void decode_words(const QDev& q, const float* lut, const CodeWords<C, QT>& w,
                                              const float (&scs)[C], int64_t base, int nch, int64_t d,
                                              float4 (&deq)[C])
 {
     const int lane = lane_id();
     const int bits = QT::bits(q);
+    const int half = 4 * (lane & 32);      // ds_bpermute byte address of lane 32 for the high halves
+    const int sh = lane & 31;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
-        deq[ch] = zero4();
-        if (ch >= nch) continue;
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
         const float sc = uniform(scs[ch]);
-        const bool ok = !scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc));
-        const uint32_t lo = (uint32_t)wv[ch], hi = (uint32_t)(wv[ch] >> 32);
+        const bool ok = ch < nch && (!scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc)));
         const int nv = nvalid4(n, d);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             uint32_t cc = 0;
             for (int pl = 0; pl < bits; ++pl) {
                 const int j = k * bits + pl;
-                const uint32_t wl = (uint32_t)__builtin_amdgcn_readlane((int)lo, j);
-                const uint32_t wh = (uint32_t)__builtin_amdgcn_readlane((int)hi, j);
-                cc |= (((lane < 32 ? wl : wh) >> (lane & 31)) & 1u) << pl;
+                const uint32_t src = (CodeWords<C, QT>::R > 1 && j >= 32) ? w.x[ch][CodeWords<C, QT>::R - 1]
+                                                                          : w.x[ch][0];
+                const uint32_t h = (uint32_t)__builtin_amdgcn_ds_bpermute(half + 4 * (j & 31), (int)src);
+                // rotate bit sh of h to bit pl, then insert it
+                cc |= __builtin_amdgcn_alignbit(h, h, (uint32_t)(sh - pl) & 31u) & (1u << pl);
             }
-            const float dv = ok ? deq_of<QT>(q, lut, cc, 0.0f, sc) : 0.0f;
-            set_comp(deq[ch], k, k < nv ? dv : 0.0f);
+            const float dv = deq_of<QT>(q, lut, cc, 0.0f, sc);
+            set_comp(deq[ch], k, ok && k < nv ? dv : 0.0f);
         }
     }
 }
@@ -700,7 +733,7 @@ __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, co
         return;
     }
     if (plane_coded<QT>(q)) {
-        uint64_t wv[C];
+        CodeWords<C, QT> wv;
         float sc[C];
         load_code_words<C, QT>(q, codes, base, nch, wv);
         load_chunk_scales<C, QT>(q, scales, base, nch, sc);
@@ -1096,7 +1129,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
     // Bit-plane messages: the next worker's code words and scales are loaded
     // while the current worker's are decoded.
     const bool planes = plane_coded<QW>(a.qw);
-    uint64_t wv[C];
+    CodeWords<C, QW> wv;
     float sc[C];
     if (planes) {
         load_code_words<C, QW>(a.qw, a.wcodes, t.base, t.nch, wv);
@@ -1105,16 +1138,14 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
     for (int i = 0; i < a.N; ++i) {
         if (planes) {
             const int64_t j = i + 1 < a.N ? i + 1 : i;
-            uint64_t nwv[C];
+            CodeWords<C, QW> nwv;
             float nsc[C];
             load_code_words<C, QW>(a.qw, a.wcodes + j * a.qw.words, t.base, t.nch, nwv);
             load_chunk_scales<C, QW>(a.qw, a.wscales + j * a.qw.nscales, t.base, t.nch, nsc);
             decode_words<C, QW>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, dq);
+            wv = nwv;
 #pragma unroll
-            for (int ch = 0; ch < C; ++ch) {
-                wv[ch] = nwv[ch];
-                sc[ch] = nsc[ch];
-            }
+            for (int ch = 0; ch < C; ++ch) sc[ch] = nsc[ch];
         } else {
             dequant_tile<C, QW>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
                                  a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, dq);

@@ -117,6 +117,15 @@ def test_quantizer_kinds(kind):
     _run(4 * 1024 + 260, 3, q, q, O.ADAM_AT_SERVER, T=5, gen="outliers")
 
 
+@pytest.mark.parametrize("kind", list(KINDS))
+def test_quantizer_kinds_split_calls(kind):
+    """Every code width through the split calls, whose messages are decoded
+    from HBM (9-bit codes span two registers of spread words)."""
+    q = KINDS[kind]
+    _run(4 * 1024 + 260, 3, q, q, O.ADAM_AT_WORKER, T=4, gen="outliers", split=True)
+    _run(2 * 1024 + 700, 5, q, SIGN(512), O.ADAM_AT_SERVER, T=4, gen="outliers", split=True)
+
+
 @pytest.mark.parametrize("ef", [(0, 0), (0, 1), (1, 0)], ids=["off-off", "off-on", "on-off"])
 def test_error_feedback_switches(ef):
     _run(3000, 4, STOCH(2, O.SCALE_MAX, 512, ef[0]), SIGN(1024, ef[1]), O.ADAM_AT_SERVER, T=5)
