@@ -112,13 +112,14 @@ template <int C, bool VEC>
 __global__ __launch_bounds__(kBlock) void apply_kernel(StepArgs a)
 {
     __shared__ float lut_s[kLutSize];
+    __shared__ __attribute__((aligned(16))) uint32_t stage_all[kWavesPerBlock][stage_words<C, QRt>()];
     fill_lut(a.qs, lut_s);
     __syncthreads();
     TilePos t;
     if (!tile_pos<C>(a, t)) return;
     const int lane = lane_id();
     float4 dq[C];
-    dequant_tile<C, QRt>(a.qs, lut_s, a.scodes, a.sscales, t.base, t.nch, a.d, dq);
+    dequant_tile<C, QRt>(a.qs, lut_s, a.scodes, a.sscales, t.base, t.nch, a.d, stage_all[threadIdx.x / kWave], dq);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         if (ch >= t.nch) continue;

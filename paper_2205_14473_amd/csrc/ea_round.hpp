@@ -601,8 +601,8 @@ __host__ __device__ constexpr int max_code_bits()
 // `lane` of a word lies in its low half for lanes 0-31 and in its high half
 // for lanes 32-63; of each chunk's 4*bits words, lane l holds that half of
 // word l mod 32 (x[ch][0]) and, for codes wider than 8 bits, of word
-// 32 + l mod 32 (x[ch][1]).  A decoding lane fetches the half it needs from
-// the lane that holds it (ds_bpermute).  Lanes past a chunk's words, and
+// 32 + l mod 32 (x[ch][1]).  Written to LDS in that order, the halves a
+// lane needs are consecutive (decode_words).  Lanes past a chunk's words, and
 // chunks past the tile's end, load a word that exists and decode to nothing:
 // the loads take no branch, so the next worker's words stay in flight while
 // the current worker's are decoded.  (The select on the chunk count also
@@ -649,31 +649,67 @@ __device__ __forceinline__ void load_chunk_scales(const QDev& q, const float* __
     }
 }
 
+// LDS a wave needs to decode a tile (decode_words): the spread words of its
+// chunks.
+template <int C, class QT>
+__host__ __device__ constexpr int stage_words()
+{
+    return C * CodeWords<C, QT>::R * kWave;
+}
+
 // Decode one tile from its spread code words (load_code_words) and chunk
-// scales: bit p of the code of slot k is bit `lane` of word k*bits + p.
+// scales: bit p of the code of slot k is bit `lane` of word k*bits + p.  The
+// wave writes its words to `stage` (stage_words() dwords of its own) and reads
+// back the halves that hold its bits, four words per 16-byte read; a rotate
+// moves each bit to its place in the code.  One wave's LDS accesses complete
+// in order, so only the compiler has to be kept from reordering them.
 template <int C, class QT>
 __device__ __forceinline__ void decode_words(const QDev& q, const float* lut, const CodeWords<C, QT>& w,
                                              const float (&scs)[C], int64_t base, int nch, int64_t d,
-                                             float4 (&deq)[C])
+                                             uint32_t* stage, float4 (&deq)[C])
 {
+    constexpr int R = CodeWords<C, QT>::R;
     const int lane = lane_id();
     const int bits = QT::bits(q);
-    const int half = 4 * (lane & 32);      // ds_bpermute byte address of lane 32 for the high halves
+    const int nw = 4 * bits;
     const int sh = lane & 31;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch)
+#pragma unroll
+        for (int r = 0; r < R; ++r) stage[(ch * R + r) * kWave + lane] = w.x[ch][r];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
         const float sc = uniform(scs[ch]);
         const bool ok = ch < nch && (!scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc)));
         const int nv = nvalid4(n, d);
+        // this lane's halves of the chunk's words (with the code width known
+        // at compile time; else read one at a time below)
+        const uint32_t* sl = stage + ch * R * kWave + (lane & 32);
+        uint32_t hw[R * 32];
+#pragma unroll
+        for (int j4 = 0; j4 < R * 32; j4 += 4) {
+            if (QT::fixed && j4 < nw) {
+                const uint4 v = *reinterpret_cast<const uint4*>(sl + (j4 >> 5) * kWave + (j4 & 31));
+                hw[j4] = v.x;
+                hw[j4 + 1] = v.y;
+                hw[j4 + 2] = v.z;
+                hw[j4 + 3] = v.w;
+            }
+        }
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             uint32_t cc = 0;
-            for (int pl = 0; pl < bits; ++pl) {
+#pragma unroll
+            for (int pl = 0; pl < max_code_bits<QT>(); ++pl) {
+                if (pl >= bits) break;
                 const int j = k * bits + pl;
-                const uint32_t src = (CodeWords<C, QT>::R > 1 && j >= 32) ? w.x[ch][CodeWords<C, QT>::R - 1]
-                                                                          : w.x[ch][0];
-                const uint32_t h = (uint32_t)__builtin_amdgcn_ds_bpermute(half + 4 * (j & 31), (int)src);
+                const uint32_t h = QT::fixed ? hw[j] : sl[(j >> 5) * kWave + (j & 31)];
                 // rotate bit sh of h to bit pl, then insert it
                 cc |= __builtin_amdgcn_alignbit(h, h, (uint32_t)(sh - pl) & 31u) & (1u << pl);
             }
@@ -695,7 +731,7 @@ __device__ __forceinline__ bool plane_coded(const QDev& q)
 template <int C, class QT>
 __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, const uint64_t* __restrict__ codes,
                                              const float* __restrict__ scales, int64_t base, int nch, int64_t d,
-                                             float4 (&deq)[C])
+                                             uint32_t* stage, float4 (&deq)[C])
 {
     const int lane = lane_id();
     if (is_sparse<QT>(q)) {
@@ -737,7 +773,7 @@ __device__ __forceinline__ void dequant_tile(const QDev& q, const float* lut, co
         float sc[C];
         load_code_words<C, QT>(q, codes, base, nch, wv);
         load_chunk_scales<C, QT>(q, scales, base, nch, sc);
-        decode_words<C, QT>(q, lut, wv, sc, base, nch, d, deq);
+        decode_words<C, QT>(q, lut, wv, sc, base, nch, d, stage, deq);
         return;
     }
 #pragma unroll
@@ -1116,10 +1152,12 @@ template <int C, bool VEC, class QW = QRt>
 __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
 {
     __shared__ float lut_w[kLutSize];
+    __shared__ __attribute__((aligned(16))) uint32_t stage_all[kWavesPerBlock][stage_words<C, QW>()];
     fill_lut(a.qw, lut_w);
     __syncthreads();
     TilePos t;
     if (!tile_pos<C>(a, t)) return;
+    uint32_t* stage = stage_all[threadIdx.x / kWave];
     const int lane = lane_id();
     float4 acc[C], dq[C], u[C];
     ServerRows<C> sr;
@@ -1142,13 +1180,13 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
             float nsc[C];
             load_code_words<C, QW>(a.qw, a.wcodes + j * a.qw.words, t.base, t.nch, nwv);
             load_chunk_scales<C, QW>(a.qw, a.wscales + j * a.qw.nscales, t.base, t.nch, nsc);
-            decode_words<C, QW>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, dq);
+            decode_words<C, QW>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, stage, dq);
             wv = nwv;
 #pragma unroll
             for (int ch = 0; ch < C; ++ch) sc[ch] = nsc[ch];
         } else {
             dequant_tile<C, QW>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
-                                 a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, dq);
+                                 a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, stage, dq);
         }
 #pragma unroll
         for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
