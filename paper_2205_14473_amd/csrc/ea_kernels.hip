@@ -73,61 +73,6 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(const double* __restri
     }
 }
 
-// Server compression from u (a.ubuf) and e_s; optionally also x -= message.
-template <int C, bool VEC>
-__global__ __launch_bounds__(kBlock) void server_kernel(StepArgs args)
-{
-    const StepArgs a = with_step(args);
-    __shared__ float lut_s[kLutSize];
-    fill_lut(a.qs, lut_s);
-    __syncthreads();
-    TilePos t;
-    if (!tile_pos<C>(a, t)) return;
-    const int lane = lane_id();
-    const bool sglobal = has_scale<QRt>(a.qs) && a.qs.cpb == 0;
-    float4 q[C], dq[C];
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        q[ch] = zero4();
-        if (ch >= t.nch) continue;
-        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        q[ch] = add4(ld4<VEC>(a.ubuf, n, a.d), ld4<VEC>(a.e_s, n, a.d));
-    }
-    const float gs = sglobal ? a.sscales[0] : 0.0f;
-    WordSink sink = message_sink<QRt>(a.qs, a.scodes, t.base);
-    quantize_tile<C, false, QRt>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, gs, a.scodes,
-                                 a.sscales, sink, dq);
-    sink.flush();
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (ch >= t.nch) continue;
-        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        st4<VEC>(a.e_s, n, a.d, a.qs.ef ? sub4(q[ch], dq[ch]) : zero4());
-        if (a.apply) st4<VEC>(a.x, n, a.d, sub4(ld4<VEC>(a.x, n, a.d), dq[ch]));
-    }
-}
-
-// Split call: x -= dequantized server message.
-template <int C, bool VEC>
-__global__ __launch_bounds__(kBlock) void apply_kernel(StepArgs a)
-{
-    __shared__ float lut_s[kLutSize];
-    __shared__ __attribute__((aligned(16))) uint32_t stage_all[kWavesPerBlock][stage_words<C, QRt>()];
-    fill_lut(a.qs, lut_s);
-    __syncthreads();
-    TilePos t;
-    if (!tile_pos<C>(a, t)) return;
-    const int lane = lane_id();
-    float4 dq[C];
-    dequant_tile<C, QRt>(a.qs, lut_s, a.scodes, a.sscales, t.base, t.nch, a.d, stage_all[threadIdx.x / kWave], dq);
-#pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (ch >= t.nch) continue;
-        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
-        st4<VEC>(a.x, n, a.d, sub4(ld4<VEC>(a.x, n, a.d), dq[ch]));
-    }
-}
-
 __global__ void fill_kernel(float* __restrict__ p, int64_t n, float value)
 {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
@@ -216,19 +161,23 @@ const Special* find_special(const StepArgs& a, int C)
 // A kernel specialized for the worker quantizer, when one matches: whole
 // tiles of one worker bucket each, or of any size for a worker quantizer
 // without buckets (Example 2, full precision).
-const HalfKernel* find_half(const StepArgs& a, int C)
+const HalfKernel* find_half_for(const QDev& q, int C)
 {
-    const bool bucketless = a.qw.kind == Q_POW2 || a.qw.kind == Q_NONE;
-    if (a.qw.cpb != (bucketless ? 0 : C)) return nullptr;
+    const bool bucketless = q.kind == Q_POW2 || q.kind == Q_NONE;
+    if (q.cpb != (bucketless ? 0 : C)) return nullptr;
     int n = 0;
     const HalfKernel* t = C == 1 ? half_kernels_c1(&n) : C == 2 ? half_kernels_c2(&n)
                         : C == 4 ? half_kernels_c4(&n) : C == 8 ? half_kernels_c8(&n) : nullptr;
     for (int i = 0; i < n; ++i) {
         const HalfKernel& h = t[i];
-        if (h.C == C && h.wkind == a.qw.kind && h.wbits == a.qw.bits && h.wnorm == a.qw.norm && h.wcpb == a.qw.cpb)
-            return &h;
+        if (h.C == C && h.wkind == q.kind && h.wbits == q.bits && h.wnorm == q.norm && h.wcpb == q.cpb) return &h;
     }
     return nullptr;
+}
+
+const HalfKernel* find_half(const StepArgs& a, int C)
+{
+    return find_half_for(a.qw, C);
 }
 
 // A fully specialized kernel for a wide tile with the same quantizer on both
@@ -352,14 +301,26 @@ hipError_t launch_aggregate(const StepArgs& a, int C, bool vec, hipStream_t s)
     return hipGetLastError();
 }
 
+// The split server calls take the worker-specialized tables' kernels for the
+// server quantizer when it is one of theirs.
 hipError_t launch_server(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
+    const HalfKernel* hk = vec ? find_half_for(a.qs, C) : nullptr;
+    if (hk) {
+        hipLaunchKernelGGL(hk->server, dim3((unsigned)grid_of(a)), dim3(kBlock), 0, s, a);
+        return hipGetLastError();
+    }
     EA_DISPATCH(server_kernel, C, vec, grid_of(a), s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_apply(const StepArgs& a, int C, bool vec, hipStream_t s)
 {
+    const HalfKernel* hk = vec ? find_half_for(a.qs, C) : nullptr;
+    if (hk) {
+        hipLaunchKernelGGL(hk->apply, dim3((unsigned)grid_of(a)), dim3(kBlock), 0, s, a);
+        return hipGetLastError();
+    }
     EA_DISPATCH(apply_kernel, C, vec, grid_of(a), s, a);
     return hipGetLastError();
 }

@@ -64,6 +64,9 @@ struct HalfKernel {
     int tiles;                // tiles per block
     void (*worker)(StepArgs);     // split call: one worker's compression (aligned rows)
     void (*aggregate)(StepArgs);  // split call: decode and average of the N messages
+    // The same quantizer on the server side of the split calls (aligned rows):
+    void (*server)(StepArgs);     // the server's compression
+    void (*apply)(StepArgs);      // x -= the server message
 };
 // Fully specialized fused-round kernels for the same quantizer on both sides
 // with Adam at the server, for wide tiles (C = 4, 8), where a run-time server

@@ -1200,6 +1200,62 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
 }
 
 
+// Split call: the server's compression of u (a.ubuf) plus e_s; with a.apply
+// also x -= its message.  QS: the server quantizer's traits.
+template <int C, bool VEC, class QS = QRt>
+__global__ __launch_bounds__(kBlock) void server_kernel(StepArgs args)
+{
+    const StepArgs a = with_step(args);
+    __shared__ float lut_s[kLutSize];
+    fill_lut(a.qs, lut_s);
+    __syncthreads();
+    TilePos t;
+    if (!tile_pos<C>(a, t)) return;
+    const int lane = lane_id();
+    const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
+    float4 q[C], dq[C];
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        q[ch] = zero4();
+        if (ch >= t.nch) continue;
+        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
+        q[ch] = add4(ld4<VEC>(a.ubuf, n, a.d), ld4<VEC>(a.e_s, n, a.d));
+    }
+    const float gs = sglobal ? a.sscales[0] : 0.0f;
+    WordSink sink = message_sink<QS>(a.qs, a.scodes, t.base);
+    quantize_tile<C, false, QS>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, gs, a.scodes,
+                                a.sscales, sink, dq);
+    sink.flush();
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        if (ch >= t.nch) continue;
+        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
+        st4<VEC>(a.e_s, n, a.d, a.qs.ef ? sub4(q[ch], dq[ch]) : zero4());
+        if (a.apply) st4<VEC>(a.x, n, a.d, sub4(ld4<VEC>(a.x, n, a.d), dq[ch]));
+    }
+}
+
+// Split call: x -= the dequantized server message.
+template <int C, bool VEC, class QS = QRt>
+__global__ __launch_bounds__(kBlock) void apply_kernel(StepArgs a)
+{
+    __shared__ float lut_s[kLutSize];
+    __shared__ __attribute__((aligned(16))) uint32_t stage_all[kWavesPerBlock][stage_words<C, QS>()];
+    fill_lut(a.qs, lut_s);
+    __syncthreads();
+    TilePos t;
+    if (!tile_pos<C>(a, t)) return;
+    const int lane = lane_id();
+    float4 dq[C];
+    dequant_tile<C, QS>(a.qs, lut_s, a.scodes, a.sscales, t.base, t.nch, a.d, stage_all[threadIdx.x / kWave], dq);
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) {
+        if (ch >= t.nch) continue;
+        const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
+        st4<VEC>(a.x, n, a.d, sub4(ld4<VEC>(a.x, n, a.d), dq[ch]));
+    }
+}
+
 // Floats of the code-table region of a fused-round block with G waves: room
 // for both block-wide tables or for two 64-entry tables per wave.
 __host__ __device__ constexpr int table_floats(int G)
