@@ -211,7 +211,7 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
     const HalfKernel* hk = vec && !sp && !sk ? find_half(a, C) : nullptr;
     if (nfull > 0) {
         const int K = sp ? sp->tiles : sk ? sk->tiles : hk ? hk->tiles : round_tiles_per_block(C, false);
-        const int G = round_waves(a.N, C, K, limit);
+        const int G = round_waves(a.N, C, K, limit, a.placement);
         StepArgs b = a;
         b.tile0 = 0;
         b.tile1 = nfull;
@@ -236,7 +236,7 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
         if (e != hipSuccess) return e;
     }
     if (nfull < a.ntiles) {
-        const int G = round_waves(a.N, C, 1, limit);
+        const int G = round_waves(a.N, C, 1, limit, a.placement);
         StepArgs b = a;
         b.tile0 = nfull;
         b.tile1 = a.ntiles;

@@ -47,6 +47,15 @@ __host__ __device__ constexpr int max_round_waves(int C)
     return C <= 2 ? EA_NARROW_TILE_WAVES : (C == 4 ? 8 : EA_WIDE_TILE_WAVES);
 }
 
+// One-chunk tiles with Adam at the server launch narrower blocks (more of
+// them per CU): a worker's tile there is little work per wave, and 16-wave
+// blocks left the CUs waiting on block boundaries (BERT-sized, 16 workers:
+// stochastic 4-bit L2 with 256-element buckets 5.95 -> 4.81 ms, top-8 of 256
+// 7.05 -> 4.88 ms).  With Adam at the workers 16 waves stay faster.
+#ifndef EA_C1_SERVER_WAVES
+#define EA_C1_SERVER_WAVES 4
+#endif
+
 // Tiles per block of the fused round.  Lean kernels (whole tiles, Adam at
 // the server) take two consecutive tiles per block; the others one.
 #ifndef EA_TILES_PER_BLOCK
@@ -1273,9 +1282,10 @@ inline size_t round_lds_bytes(int N, int C, int G, int K)
 
 // Waves per block: one per worker up to the tile's limit, fewer if the LDS
 // would exceed what a block may use.
-inline int round_waves(int N, int C, int K, size_t lds_limit)
+inline int round_waves(int N, int C, int K, size_t lds_limit, int placement)
 {
-    int G = N < max_round_waves(C) ? N : max_round_waves(C);
+    const int cap = C == 1 && placement == AT_SERVER ? EA_C1_SERVER_WAVES : max_round_waves(C);
+    int G = N < cap ? N : cap;
     while (G > 1 && round_lds_bytes(N, C, G, K) > lds_limit) G = (G + 1) / 2;
     return G;
 }
