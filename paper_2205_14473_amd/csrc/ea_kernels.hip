@@ -158,9 +158,11 @@ const Special* find_special(const StepArgs& a, int C)
     return nullptr;
 }
 
-// A kernel specialized for the worker quantizer, when one matches: whole
-// tiles of one worker bucket each, or of any size for a worker quantizer
-// without buckets (Example 2, full precision).
+// The specialized tables' entry for quantizer q at tile size C, when one
+// matches: tiles of one bucket of q each, or of any size for a quantizer
+// without buckets (Example 2, full precision).  find_half keys on the worker
+// quantizer (the fused round and the split worker calls); the split server
+// calls key on the server's.
 const HalfKernel* find_half_for(const QDev& q, int C)
 {
     const bool bucketless = q.kind == Q_POW2 || q.kind == Q_NONE;
