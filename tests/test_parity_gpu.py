@@ -177,6 +177,16 @@ def test_many_workers(N):
     _run(d, N, qfields(O.Q_DET_UNIFORM, 2, bucket=512), SIGN(1024), O.ADAM_AT_SERVER, T=2)
 
 
+@pytest.mark.parametrize("N", [3, 4, 5, 8, 17, 100])
+def test_one_chunk_tiles_worker_groups(N):
+    """One-chunk tiles with Adam at the server run blocks of at most four
+    waves, so each wave compresses several workers in turn: worker counts
+    below, at and past a multiple of four."""
+    d = 256 * 13 + 77
+    _run(d, N, STOCH(4, O.SCALE_L2, 256), STOCH(4, O.SCALE_L2, 256), O.ADAM_AT_SERVER, T=3)
+    _run(d, N, SIGN(256), qfields(O.Q_TOPK, bucket=256, keep=9), O.ADAM_AT_SERVER, T=2)
+
+
 EXTREME_KINDS = {
     "stoch4_l2": STOCH(4, O.SCALE_L2, 512),
     "stoch2_max": STOCH(2, O.SCALE_MAX, 512),
