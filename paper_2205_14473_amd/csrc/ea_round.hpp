@@ -1291,7 +1291,7 @@ inline int round_waves(int N, int C, int K, size_t lds_limit, int placement)
 }
 
 // Per-block LDS limit of the current device (queried once per device).
-size_t lds_limit_bytes()
+[[maybe_unused]] size_t lds_limit_bytes()
 {
     static size_t cached[64] = {0};
     int dev = 0;
