@@ -713,16 +713,19 @@ __device__ __forceinline__ void decode_words(const QDev& q, const float* lut, co
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            uint32_t cc = 0;
+            // the code times 4: its byte offset in the code table
+            uint32_t c4 = 0;
 #pragma unroll
             for (int pl = 0; pl < max_code_bits<QT>(); ++pl) {
                 if (pl >= bits) break;
                 const int j = k * bits + pl;
                 const uint32_t h = QT::fixed ? hw[j] : sl[(j >> 5) * kWave + (j & 31)];
-                // rotate bit sh of h to bit pl, then insert it
-                cc |= __builtin_amdgcn_alignbit(h, h, (uint32_t)(sh - pl) & 31u) & (1u << pl);
+                // rotate bit sh of h to bit pl + 2, then insert it
+                c4 |= __builtin_amdgcn_alignbit(h, h, (uint32_t)(sh - pl - 2) & 31u) & (4u << pl);
             }
-            const float dv = deq_of<QT>(q, lut, cc, 0.0f, sc);
+            const float tv = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(lut) + c4);
+            const int kind = QT::kind(q);
+            const float dv = kind == Q_SCALED_SIGN ? (c4 ? -sc : sc) : (kind == Q_POW2 ? tv : sc * tv);
             set_comp(deq[ch], k, ok && k < nv ? dv : 0.0f);
         }
     }
