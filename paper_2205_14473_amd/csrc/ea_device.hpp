@@ -264,9 +264,11 @@ __device__ __forceinline__ float lut_entry(const QDev& q, int32_t c)
 }
 
 // Whole-block table (any code width); the caller synchronizes the block.
+// Only the 2^bits entries a code can select are filled.
 __device__ __forceinline__ void fill_lut(const QDev& q, float* lut)
 {
-    for (int c = threadIdx.x; c < kLutSize; c += blockDim.x) lut[c] = lut_entry<QRt>(q, c);
+    const int n = q.bits < 9 ? (1 << q.bits) : kLutSize;
+    for (int c = threadIdx.x; c < n; c += blockDim.x) lut[c] = lut_entry<QRt>(q, c);
 }
 
 // Tables of specialized quantizers with codes below 64 are built per wave:
