@@ -699,7 +699,7 @@ __host__ __device__ constexpr uint32_t dot_weights(int k, int i, bool hi)
 // each group of four bytes into four bits with a shift and a mask; a packed
 // dot product (v_dot4_u32_u8) then weighs the plane bits of a code straight
 // into its byte offset in the code table.
-template <int C, class QT>
+template <int C, class QT, bool SUM>
 __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lut, const CodeWords<C, QT>& w,
                                                   const float (&scs)[C], int64_t base, int nch, int64_t d,
                                                   uint32_t* stage, float4 (&deq)[C])
@@ -734,6 +734,7 @@ __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lu
         const float sc = uniform(scs[ch]);
         const bool ok = ch < nch && (!scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc)));
         const int nv = nvalid4(n, d);
+        const float se = ok ? sc : 0.0f;
         // the lane's row: B dwords of four word-bytes each, reduced to the
         // lane's bit of each byte
         const uint32_t* row = reinterpret_cast<const uint32_t*>(sb + (ch * 8 + (lane >> 3)) * RS);
@@ -760,8 +761,9 @@ __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lu
             const uint32_t c4 = lo + (hi << 8);
             const float tv = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(lut) + c4);
             const int kind = QT::kind(q);
-            const float dv = kind == Q_SCALED_SIGN ? (c4 ? -sc : sc) : (kind == Q_POW2 ? tv : sc * tv);
-            set_comp(deq[ch], k, ok && k < nv ? dv : 0.0f);
+            const float s = SUM ? se : sc;
+            const float dv = kind == Q_SCALED_SIGN ? (c4 ? -s : s) : (kind == Q_POW2 ? tv : s * tv);
+            set_comp(deq[ch], k, SUM || (ok && k < nv) ? dv : 0.0f);
         }
     }
 }
@@ -772,7 +774,12 @@ __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lu
 // back the halves that hold its bits, four words per 16-byte read; a rotate
 // moves each bit to its place in the code.  One wave's LDS accesses complete
 // in order, so only the compiler has to be kept from reordering them.
-template <int C, class QT>
+//
+// SUM: the caller only adds the values to sums that start at +0 and never
+// stores the lanes past d.  A gated bucket (zero or non-finite scale) then
+// decodes to zeros of either sign, which leave such a sum's bits as +0 would,
+// and the lanes past d or past the tile are not masked: no select per element.
+template <int C, class QT, bool SUM = false>
 __device__ __forceinline__ void decode_words(const QDev& q, const float* lut, const CodeWords<C, QT>& w,
                                              const float (&scs)[C], int64_t base, int nch, int64_t d,
                                              uint32_t* stage, float4 (&deq)[C])
@@ -782,7 +789,7 @@ __device__ __forceinline__ void decode_words(const QDev& q, const float* lut, co
     // than writing bytes (ResNet-18-sized sign, 2048-element buckets: 58 against
     // 64 us).
     if constexpr (QT::fixed && max_code_bits<QT>() >= 2) {
-        decode_words_rows<C, QT>(q, lut, w, scs, base, nch, d, stage, deq);
+        decode_words_rows<C, QT, SUM>(q, lut, w, scs, base, nch, d, stage, deq);
         return;
     }
     constexpr int R = CodeWords<C, QT>::R;
@@ -833,8 +840,9 @@ __device__ __forceinline__ void decode_words(const QDev& q, const float* lut, co
             }
             const float tv = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(lut) + c4);
             const int kind = QT::kind(q);
-            const float dv = kind == Q_SCALED_SIGN ? (c4 ? -sc : sc) : (kind == Q_POW2 ? tv : sc * tv);
-            set_comp(deq[ch], k, ok && k < nv ? dv : 0.0f);
+            const float s = SUM ? (ok ? sc : 0.0f) : sc;
+            const float dv = kind == Q_SCALED_SIGN ? (c4 ? -s : s) : (kind == Q_POW2 ? tv : s * tv);
+            set_comp(deq[ch], k, SUM || (ok && k < nv) ? dv : 0.0f);
         }
     }
 }
@@ -1298,7 +1306,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
             float nsc[C];
             load_code_words<C, QW>(a.qw, a.wcodes + j * a.qw.words, t.base, t.nch, nwv);
             load_chunk_scales<C, QW>(a.qw, a.wscales + j * a.qw.nscales, t.base, t.nch, nsc);
-            decode_words<C, QW>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, stage, dq);
+            decode_words<C, QW, true>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, stage, dq);
             wv = nwv;
 #pragma unroll
             for (int ch = 0; ch < C; ++ch) sc[ch] = nsc[ch];
