@@ -248,6 +248,10 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
             hipLaunchKernelGGL(sp->edge, grid, block, lds, s, b);
             return hipGetLastError();
         }
+        if (sk) {
+            hipLaunchKernelGGL(sk->edge, grid, block, lds, s, b);
+            return hipGetLastError();
+        }
         switch (C) {
         case 1: hipLaunchKernelGGL((step_kernel<1, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
         case 2: hipLaunchKernelGGL((step_kernel<2, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;

@@ -75,6 +75,7 @@ struct SymKernel {
     int C, kind, bits, norm, cpb;
     void (*kernel)(StepArgs);
     int tiles;
+    void (*edge)(StepArgs);   // the last, partial tile (aligned rows)
 };
 const SymKernel* sym_kernels_c4(int* n);
 const SymKernel* sym_kernels_c8(int* n);

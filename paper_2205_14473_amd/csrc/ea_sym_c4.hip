@@ -14,7 +14,8 @@ template <class Q>
 constexpr SymKernel sym()
 {
     return SymKernel{4, Q::kind(QDev{}), Q::bits(QDev{}), Q::norm(QDev{}), Q::cpb(QDev{}),
-                     step_kernel<4, true, true, Q, Q, AT_SERVER>, round_tiles_per_block(4, true)};
+                     step_kernel<4, true, true, Q, Q, AT_SERVER>, round_tiles_per_block(4, true),
+                     step_kernel<4, true, false, Q, Q, AT_SERVER>};
 }
 
 const SymKernel kSym[] = {

@@ -22,7 +22,7 @@ constexpr SymKernel sym()
 {
     return SymKernel{8, Q::kind(QDev{}), Q::bits(QDev{}), Q::norm(QDev{}), Q::cpb(QDev{}),
                      step_kernel<8, true, true, Q, Q, AT_SERVER, EA_SYM_C8_MIN_WAVES>,
-                     round_tiles_per_block(8, true)};
+                     round_tiles_per_block(8, true), step_kernel<8, true, false, Q, Q, AT_SERVER, EA_SYM_C8_MIN_WAVES>};
 }
 
 const SymKernel kSym[] = {
