@@ -92,15 +92,17 @@ def test_full_size_sampled(key):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("key", ["bert", "gpt2m", "resnet50", "bert_topk"])
-def test_full_size_split_calls_equal_fused(key):
+@pytest.mark.parametrize("key,placement", [("bert", None), ("gpt2m", None), ("resnet50", None), ("bert_topk", None),
+                                           ("bert", O.ADAM_AT_WORKER)])
+def test_full_size_split_calls_equal_fused(key, placement):
     """The four split calls at full size give, output for output, the same
     bits as ea_step: both sum the workers in ascending order and run the same
     element steps, so any difference is a decoding or indexing fault at a
     size the reduced-size parity cases do not reach."""
     w = W.WORKLOADS[key]
-    print(f"\n[fullsize split] {w.name}", flush=True)
-    _, ec = configs(w.d, w.N, w.qw.fields(), w.qs.fields(), w.placement, w.seed, w.beta1, w.beta2, w.lr, w.eps)
+    pl = w.placement if placement is None else placement
+    print(f"\n[fullsize split] {w.name} placement={pl}", flush=True)
+    _, ec = configs(w.d, w.N, w.qw.fields(), w.qs.fields(), pl, w.seed, w.beta1, w.beta2, w.lr, w.eps)
     a, b = allocate(ec), allocate(ec, with_u=True)
     init_state(ec, a)
     init_state(ec, b)
@@ -110,14 +112,17 @@ def test_full_size_split_calls_equal_fused(key):
         E.ea_step(ec, t, **a.step_args())
         b.g.copy_(a.g)
         for i in range(w.N):
-            E.ea_worker_compress(ec, i, t, b.g[i], b.e_w[i], None, None, b.wcodes[i],
+            E.ea_worker_compress(ec, i, t, b.g[i], b.e_w[i], None if b.m_w is None else b.m_w[i],
+                                 None if b.v_w is None else b.v_w[i], b.wcodes[i],
                                  b.wscales[i] if nsw else None, b.workspace)
         E.ea_server_aggregate_adam(ec, t, b.wcodes, b.wscales if nsw else None, b.m, b.v, b.u)
         E.ea_server_compress(ec, t, b.u, b.e_s, b.scodes, b.sscales if nss else None, b.workspace)
         E.ea_worker_apply(ec, b.scodes, b.sscales if nss else None, b.x)
         torch.cuda.synchronize()
-        for k in ("wcodes", "wscales", "scodes", "sscales", "e_w", "e_s", "m", "v", "x"):
+        for k in ("wcodes", "wscales", "scodes", "sscales", "e_w", "e_s", "m", "v", "m_w", "v_w", "x"):
             x, y = getattr(a, k), getattr(b, k)
+            if x is None:
+                continue
             assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), f"{key} step {t}: {k} differs"
     print(f"[fullsize split] {key}: bit-identical over 2 steps", flush=True)
     del a, b
