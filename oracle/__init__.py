@@ -11,6 +11,6 @@ from .eao import (  # noqa: F401
     SCALE_L1, SCALE_L2, SCALE_MAX, ADAM_AT_SERVER, ADAM_AT_WORKER,
     SCHED_CONSTANT, SCHED_ASSUMPTION2, SCHED_STEP_DECAY, Schedule, schedule_at, toy_grad,
     Quant, Config, lib, philox, uniforms, code_bits, bucket_len, num_scales,
-    msg_words, quantize, dequantize, pack, unpack, adam_moments, adam_update,
+    msg_words, quantize, quantize_bucket, dequantize, pack, unpack, adam_moments, adam_update,
     State, step,
 )

@@ -9,29 +9,40 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "liboracle.so")
+SAN_LIB = os.path.join(HERE, "liboracle_san.so")
 SOURCES = [os.path.join(HERE, "eao.c")]
 CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
           "-fno-fast-math", "-fno-strict-aliasing", "-Wall", "-Wextra"]
+# The same source checked by AddressSanitizer and UndefinedBehaviorSanitizer
+# (with float-to-integer overflow, which -fsanitize=undefined leaves out);
+# any finding aborts.  Loaded instead of LIB when EAO_SANITIZE=1, into a
+# process that preloads the sanitizer runtimes.
+SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fsanitize=float-cast-overflow", "-fno-sanitize-recover=all"]
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, sanitize: bool = False) -> str:
     """Compile the oracle; returns the path of the shared object."""
-    cmd = ["gcc", *CFLAGS, *SOURCES, "-lm", "-o", LIB + ".tmp"]
+    out = SAN_LIB if sanitize else LIB
+    flags = [f for f in CFLAGS if not (sanitize and f == "-O2")] + (SAN_FLAGS if sanitize else [])
+    cmd = ["gcc", *flags, *SOURCES, "-lm", "-o", out + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(out + ".tmp", out)
+    return out
 
 
 def ensure_built() -> str:
     """Build only when the shared object is missing or older than a source."""
-    if os.path.exists(LIB):
-        t = os.path.getmtime(LIB)
+    sanitize = os.environ.get("EAO_SANITIZE") == "1"
+    lib = SAN_LIB if sanitize else LIB
+    if os.path.exists(lib):
+        t = os.path.getmtime(lib)
         srcs = SOURCES + [os.path.join(HERE, "eao.h")]
         if all(os.path.getmtime(s) <= t for s in srcs):
-            return LIB
-    return build()
+            return lib
+    return build(sanitize=sanitize)
 
 
 if __name__ == "__main__":

@@ -159,13 +159,39 @@ static float max_abs(const float *p, int64_t n)
     return m;
 }
 
+/* Scale of one bucket of n elements: the mean absolute value (scaled sign),
+ * the max-norm (stochastic uniform with EAO_SCALE_MAX; Example 1's
+ * Q1(||x||_inf), Q1 being the identity on binary32) or the L2 norm
+ * (stochastic uniform with EAO_SCALE_L2).  Kinds without a scale give 1. */
+static float bucket_scale(const eao_quant *q, int64_t n, const float *p)
+{
+    switch (q->kind) {
+    case EAO_Q_SCALED_SIGN:
+        return (float)(sum_abs(p, n) / (double)n);
+    case EAO_Q_STOCH_UNIFORM:
+        return q->scale == EAO_SCALE_MAX ? max_abs(p, n) : sqrtf((float)sum_sq(p, n));
+    case EAO_Q_DET_UNIFORM:
+        return max_abs(p, n);
+    default:
+        return 1.0f;
+    }
+}
+
+/* Factor applied to both x and s before x/s is formed as x * (1/s): 1 for a
+ * normal scale; 2^64 (exact for both) for a scale below 2^-126, whose
+ * reciprocal would overflow.  The max-norm of a bucket of subnormal values is
+ * such a scale; an L2 norm never is (the square root of the smallest
+ * subnormal is about 3.7e-23). */
+static float prescale_of(float s)
+{
+    return s < 0x1p-126f ? 0x1p64f : 1.0f;
+}
+
 /* Scaled sign (a Definition 3 compressor): every element of a bucket is sent
  * as +-s with s the mean absolute value of the bucket.  Code 1 means negative;
  * a zero is sent as +s. */
-static void q_scaled_sign(int64_t n, const float *p, uint32_t *code, float *deq, float *scale)
+static void q_scaled_sign(int64_t n, const float *p, float s, uint32_t *code, float *deq)
 {
-    const float s = (float)(sum_abs(p, n) / (double)n);
-    *scale = s;
     for (int64_t j = 0; j < n; ++j) {
         code[j] = p[j] < 0.0f ? 1u : 0u;
         deq[j] = code[j] ? -s : s;
@@ -184,27 +210,24 @@ static float uniform_level(uint32_t c, uint32_t L)
  * lower level, so that E[Q(p)] = p.  s is the bucket's max-norm or L2-norm;
  * both bound |p|, so p/s lies in [-1, 1].  A bucket whose scale is zero or not
  * finite is sent as all zeros. */
-static void q_stoch_uniform(const eao_quant *q, int64_t n, const float *p, const float *u,
-                            uint32_t *code, float *deq, float *scale)
+static void q_stoch_uniform(const eao_quant *q, int64_t n, const float *p, const float *u, float s,
+                            uint32_t *code, float *deq)
 {
     const uint32_t L = (1u << q->bits) - 1u;
-    float s;
-    if (q->scale == EAO_SCALE_MAX) s = max_abs(p, n);
-    else s = sqrtf((float)sum_sq(p, n));
-    *scale = s;
     if (!(s > 0.0f) || isinf(s)) {
         for (int64_t j = 0; j < n; ++j) { code[j] = 0; deq[j] = 0.0f; }
         return;
     }
-    const float inv = 1.0f / s;
+    const float f = prescale_of(s);
+    const float inv = 1.0f / (s * f);
     const float h = (float)L * 0.5f;
     for (int64_t j = 0; j < n; ++j) {
-        float y = (p[j] * inv + 1.0f) * h;
+        float y = ((p[j] * f) * inv + 1.0f) * h;
         if (y < 0.0f) y = 0.0f;
         if (y > (float)L) y = (float)L;
         const float lo = floorf(y);
-        const float f = y - lo;
-        uint32_t c = (uint32_t)lo + (u[j] < f ? 1u : 0u);
+        const float fr = y - lo;
+        uint32_t c = (uint32_t)lo + (u[j] < fr ? 1u : 0u);
         if (c > L) c = L;
         code[j] = c;
         deq[j] = s * uniform_level(c, L);
@@ -214,23 +237,23 @@ static void q_stoch_uniform(const eao_quant *q, int64_t n, const float *p, const
 /* Example 1: Q(x) = Q1(|x|_inf) * Q2(x / Q1(|x|_inf)), Q2 rounding each
  * coordinate to the nearest of i/(2^k-1), i = -(2^k-1)..(2^k-1); Q(x) = 0 when
  * the max-norm is 0.  Applied per bucket.  Q1 is the identity because the
- * max-norm of binary32 values is a binary32 value.  x/s is formed as x*(1/s).
- * A coordinate exactly half-way between two levels goes to the one nearer 0
- * (the flooring direction of Remark 1).  Code c = i + (2^k - 1). */
-static void q_det_uniform(const eao_quant *q, int64_t n, const float *p,
-                          uint32_t *code, float *deq, float *scale)
+ * max-norm of binary32 values is a binary32 value.  x/s is formed as x*(1/s)
+ * (after prescale_of).  A coordinate exactly half-way between two levels goes
+ * to the one nearer 0 (the flooring direction of Remark 1).
+ * Code c = i + (2^k - 1). */
+static void q_det_uniform(const eao_quant *q, int64_t n, const float *p, float s,
+                          uint32_t *code, float *deq)
 {
     const int32_t k = q->bits - 1;
     const int32_t L = (1 << k) - 1;
-    const float s = max_abs(p, n);
-    *scale = s;
     if (!(s > 0.0f) || isinf(s)) {
         for (int64_t j = 0; j < n; ++j) { code[j] = (uint32_t)L; deq[j] = 0.0f; }
         return;
     }
-    const float inv = 1.0f / s;
+    const float f = prescale_of(s);
+    const float inv = 1.0f / (s * f);
     for (int64_t j = 0; j < n; ++j) {
-        float a = fabsf(p[j]) * inv * (float)L;
+        float a = (fabsf(p[j]) * f) * inv * (float)L;
         if (a > (float)L) a = (float)L;
         int32_t i = (int32_t)floorf(a);
         if (a - (float)i > 0.5f) i += 1;
@@ -330,37 +353,57 @@ static void q_none(int64_t n, const float *p, uint32_t *code, float *deq)
     }
 }
 
+/* Codes and dequantized values of one bucket of n elements under scale s. */
+static void code_bucket(const eao_quant *q, int64_t n, const float *p, const float *u, float s,
+                        uint32_t *code, float *deq)
+{
+    switch (q->kind) {
+    case EAO_Q_SCALED_SIGN:
+        q_scaled_sign(n, p, s, code, deq);
+        break;
+    case EAO_Q_STOCH_UNIFORM:
+        q_stoch_uniform(q, n, p, u, s, code, deq);
+        break;
+    default:
+        q_det_uniform(q, n, p, s, code, deq);
+        break;
+    }
+}
+
+static int valid_for_quantize(const eao_quant *q, const float *u)
+{
+    if (eao_code_bits(q) < 0) return 0;
+    if (q->kind == EAO_Q_STOCH_UNIFORM && q->scale != EAO_SCALE_L2 && q->scale != EAO_SCALE_MAX)
+        return 0;
+    if ((q->kind == EAO_Q_STOCH_UNIFORM || q->kind == EAO_Q_RANDK) && u == NULL) return 0;
+    return 1;
+}
+
 int eao_quantize(const eao_quant *q, int64_t d, int64_t len, const float *p,
                  const float *u, uint32_t *code, float *deq, float *scales)
 {
-    if (eao_code_bits(q) < 0) return -1;
-    if (q->kind == EAO_Q_STOCH_UNIFORM && q->scale != EAO_SCALE_L2 && q->scale != EAO_SCALE_MAX)
-        return -1;
-    if ((q->kind == EAO_Q_STOCH_UNIFORM || q->kind == EAO_Q_RANDK) && u == NULL) return -1;
+    if (!valid_for_quantize(q, u)) return -1;
     if (q->kind == EAO_Q_NONE) { q_none(len, p, code, deq); return 0; }
     if (q->kind == EAO_Q_POW2) { q_pow2(q, len, p, code, deq); return 0; }
     const int64_t B = eao_bucket_len(q, d);
     for (int64_t b0 = 0, bi = 0; b0 < len; b0 += B, ++bi) {
         const int64_t n = (len - b0 < B) ? (len - b0) : B;
-        switch (q->kind) {
-        case EAO_Q_SCALED_SIGN:
-            q_scaled_sign(n, p + b0, code + b0, deq + b0, &scales[bi]);
-            break;
-        case EAO_Q_STOCH_UNIFORM:
-            q_stoch_uniform(q, n, p + b0, u + b0, code + b0, deq + b0, &scales[bi]);
-            break;
-        case EAO_Q_DET_UNIFORM:
-            q_det_uniform(q, n, p + b0, code + b0, deq + b0, &scales[bi]);
-            break;
-        case EAO_Q_TOPK:
-        case EAO_Q_RANDK:
+        if (is_sparse(q)) {
             if (q_sparse(q, n, p + b0, u ? u + b0 : NULL, code + b0, deq + b0, scales + bi * q->keep))
                 return -1;
-            break;
-        default:
-            return -1;
+            continue;
         }
+        scales[bi] = bucket_scale(q, n, p + b0);
+        code_bucket(q, n, p + b0, u ? u + b0 : NULL, scales[bi], code + b0, deq + b0);
     }
+    return 0;
+}
+
+int eao_quantize_bucket(const eao_quant *q, int64_t n, const float *p, const float *u, float s,
+                        uint32_t *code, float *deq)
+{
+    if (!valid_for_quantize(q, u) || !has_scales(q) || n < 1) return -1;
+    code_bucket(q, n, p, u, s, code, deq);
     return 0;
 }
 
@@ -575,7 +618,7 @@ int eao_step(const eao_config *c, uint32_t t, int64_t n0, int64_t len,
              const float *g, float *e_w, float *m_w, float *v_w,
              float *m, float *v, float *e_s, float *x,
              uint64_t *wcodes, float *wscales, uint64_t *scodes, float *sscales,
-             float *srv_in)
+             float *srv_in, float *p_w, float *q_s)
 {
     const int64_t d = c->d;
     const int32_t N = c->N;
@@ -613,6 +656,7 @@ int eao_step(const eao_config *c, uint32_t t, int64_t n0, int64_t len,
         } else {
             for (int64_t n = 0; n < len; ++n) p[n] = gi[n] + ei[n];
         }
+        if (p_w) memcpy(p_w + (int64_t)i * len, p, (size_t)len * sizeof(float));
         if (needs_draws(&c->qw)) eao_uniforms(c->seed, t, (uint32_t)i, n0, len, u);
         if (eao_quantize(&c->qw, d, len, p, u, code, deq, wscales + (int64_t)i * scales_w)) {
             free(p); free(u); free(deq); free(acc); free(code);
@@ -636,6 +680,7 @@ int eao_step(const eao_config *c, uint32_t t, int64_t n0, int64_t len,
         if (srv_in) srv_in[n] = a;
         p[n] = a + e_s[n];
     }
+    if (q_s) memcpy(q_s, p, (size_t)len * sizeof(float));
     if (needs_draws(&c->qs)) eao_uniforms(c->seed, t, 0xFFFFFFFFu, n0, len, u);
     if (eao_quantize(&c->qs, d, len, p, u, code, deq, sscales)) {
         free(p); free(u); free(deq); free(acc); free(code);

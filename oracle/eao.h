@@ -12,7 +12,9 @@
  * to binary32), so the oracle computes in binary32 with round-to-nearest-even
  * and no contraction of a*b+c into a fused multiply-add.  Bucket sums are
  * accumulated in binary64 and rounded once.  Quantizer decisions are therefore
- * taken in binary32, the precision the kernels use.
+ * taken in binary32, the precision the kernels use.  x/s (Example 1, the
+ * stochastic quantizer) is formed as x * (1/s); for a scale below 2^-126,
+ * whose reciprocal overflows, x and s are first multiplied by 2^64 (exact).
  *
  * Parity status of each function is stated next to it; "parity unpinned"
  * marks a function that no test pins to something other than itself.
@@ -103,6 +105,15 @@ int64_t eao_msg_words(const eao_quant *q, int64_t len);
 int eao_quantize(const eao_quant *q, int64_t d, int64_t len, const float *p,
                  const float *u, uint32_t *code, float *deq, float *scales);
 
+/* One bucket of n elements of a scaled quantizer (SCALED_SIGN,
+ * STOCH_UNIFORM, DET_UNIFORM) coded under a given scale s instead of its own
+ * norm: the codes and dequantized values eao_quantize would give if the
+ * bucket's scale were s.  Test infrastructure for checking a result formed
+ * under a scale that differs from the oracle's in its last place.  Returns 0,
+ * or -1 on an invalid description. */
+int eao_quantize_bucket(const eao_quant *q, int64_t n, const float *p, const float *u, float s,
+                        uint32_t *code, float *deq);
+
 /* Dequantize codes back to values (inverse map of the code table). */
 int eao_dequantize(const eao_quant *q, int64_t d, int64_t len, const uint32_t *code,
                    const float *scales, float *deq);
@@ -168,13 +179,17 @@ void eao_toy_grad(int64_t d, int32_t N, const float *A, const float *x_star, con
  *   scodes, sscales   [...]      server message (out)
  *   srv_in            [len]      optional (NULL to skip): the value the server
  *                                quantizes before adding e_s
+ *   p_w               [N][len]   optional (NULL to skip): each worker's
+ *                                quantizer input p (after its residual is added)
+ *   q_s               [len]      optional (NULL to skip): the server's quantizer
+ *                                input (srv_in + e_s)
  * n0 must be a multiple of 256 and of both bucket lengths; a one-bucket
  * quantizer requires n0 == 0 and len == d.  Returns 0, or -1 on bad input. */
 int eao_step(const eao_config *c, uint32_t t, int64_t n0, int64_t len,
              const float *g, float *e_w, float *m_w, float *v_w,
              float *m, float *v, float *e_s, float *x,
              uint64_t *wcodes, float *wscales, uint64_t *scodes, float *sscales,
-             float *srv_in);
+             float *srv_in, float *p_w, float *q_s);
 
 #ifdef __cplusplus
 }

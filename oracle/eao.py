@@ -58,6 +58,8 @@ def lib():
         L.eao_msg_words.restype = C.c_int64
         L.eao_quantize.argtypes = [C.POINTER(Quant), C.c_int64, C.c_int64, P, P, P, P, P]
         L.eao_quantize.restype = C.c_int
+        L.eao_quantize_bucket.argtypes = [C.POINTER(Quant), C.c_int64, P, P, C.c_float, P, P]
+        L.eao_quantize_bucket.restype = C.c_int
         L.eao_dequantize.argtypes = [C.POINTER(Quant), C.c_int64, C.c_int64, P, P, P]
         L.eao_dequantize.restype = C.c_int
         L.eao_pack.argtypes = [C.c_int32, C.c_int64, P, P]
@@ -65,7 +67,7 @@ def lib():
         L.eao_adam_moments.argtypes = [C.c_float, C.c_float, P, P, C.c_float]
         L.eao_adam_update.argtypes = [C.c_float, C.c_float, C.c_float]
         L.eao_adam_update.restype = C.c_float
-        L.eao_step.argtypes = [C.POINTER(Config), C.c_uint32, C.c_int64, C.c_int64] + [P] * 13
+        L.eao_step.argtypes = [C.POINTER(Config), C.c_uint32, C.c_int64, C.c_int64] + [P] * 15
         L.eao_step.restype = C.c_int
         L.eao_schedule_at.argtypes = [C.POINTER(Schedule), C.c_float, C.c_float, C.c_int64, P, P]
         L.eao_schedule_at.restype = C.c_int
@@ -125,6 +127,21 @@ def quantize(q: Quant, p: np.ndarray, d: Optional[int] = None, u: Optional[np.nd
     if rc != 0:
         raise ValueError("eao_quantize rejected the quantizer description")
     return codes, deq, scales[:num_scales(q, d, n)]
+
+
+def quantize_bucket(q: Quant, p: np.ndarray, scale: float, u: Optional[np.ndarray] = None):
+    """One bucket coded under the given scale instead of its own norm;
+    returns (codes, deq)."""
+    p = np.ascontiguousarray(p, dtype=np.float32)
+    codes = np.zeros(p.size, np.uint32)
+    deq = np.zeros(p.size, np.float32)
+    if u is not None:
+        u = np.ascontiguousarray(u, dtype=np.float32)
+    rc = lib().eao_quantize_bucket(C.byref(q), p.size, _ptr(p), _ptr(u), float(np.float32(scale)),
+                                   _ptr(codes), _ptr(deq))
+    if rc != 0:
+        raise ValueError("eao_quantize_bucket rejected its arguments")
+    return codes, deq
 
 
 def dequantize(q: Quant, codes: np.ndarray, scales: np.ndarray, d: Optional[int] = None) -> np.ndarray:
@@ -221,8 +238,10 @@ class State:
                      cp(self.m_w), cp(self.v_w))
 
 
-def step(cfg: Config, t: int, g: np.ndarray, st: State, n0: int = 0, want_srv_in: bool = False):
-    """One round on segment [n0, n0+len) in place; returns the messages."""
+def step(cfg: Config, t: int, g: np.ndarray, st: State, n0: int = 0, want_srv_in: bool = False,
+         want_inputs: bool = False):
+    """One round on segment [n0, n0+len) in place; returns the messages (and,
+    with want_inputs, the quantizer inputs "p_w" [N][len] and "q_s" [len])."""
     g = np.ascontiguousarray(g, dtype=np.float32)
     N = cfg.N
     length = g.shape[1]
@@ -235,11 +254,13 @@ def step(cfg: Config, t: int, g: np.ndarray, st: State, n0: int = 0, want_srv_in
         "scodes": np.zeros(sw, np.uint64),
         "sscales": np.zeros(max(nss, 1), np.float32),
         "srv_in": np.zeros(length, np.float32) if want_srv_in else None,
+        "p_w": np.zeros((N, length), np.float32) if want_inputs else None,
+        "q_s": np.zeros(length, np.float32) if want_inputs else None,
     }
     rc = lib().eao_step(C.byref(cfg), t, n0, length, _ptr(g), _ptr(st.e_w), _ptr(st.m_w), _ptr(st.v_w),
                         _ptr(st.m), _ptr(st.v), _ptr(st.e_s), _ptr(st.x),
                         _ptr(out["wcodes"]), _ptr(out["wscales"]), _ptr(out["scodes"]),
-                        _ptr(out["sscales"]), _ptr(out["srv_in"]))
+                        _ptr(out["sscales"]), _ptr(out["srv_in"]), _ptr(out["p_w"]), _ptr(out["q_s"]))
     if rc != 0:
         raise ValueError("eao_step rejected its arguments")
     out["wscales"] = out["wscales"][:, :nsw]

@@ -17,3 +17,14 @@ extern "C" void pin_philox4x32_10(const unsigned* ctr, const unsigned* key, unsi
         out[4 * i] = r.x; out[4 * i + 1] = r.y; out[4 * i + 2] = r.z; out[4 * i + 3] = r.w;
     }
 }
+
+// rocRAND's Philox4x32-10 generator state, seeded with `seed`, at
+// subsequence stream * 2^32 + t and offset n0: the successive 32-bit outputs
+// from there, each taken as a 24-bit uniform (word >> 8) * 2^-24.
+extern "C" void pin_uniforms(unsigned long long seed, unsigned t, unsigned stream, long long n0, long long len,
+                             float* out)
+{
+    rocrand_state_philox4x32_10 st;
+    rocrand_init(seed, ((unsigned long long)stream << 32) | t, (unsigned long long)n0, &st);
+    for (long long i = 0; i < len; ++i) out[i] = (float)(rocrand(&st) >> 8) * (1.0f / 16777216.0f);
+}

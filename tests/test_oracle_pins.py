@@ -40,6 +40,8 @@ def rocrand_philox(tmp_path_factory):
                     "-I/opt/rocm/include", src, "-o", so], check=True)
     lib = ctypes.CDLL(so)
     lib.pin_philox4x32_10.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_long]
+    lib.pin_uniforms.argtypes = [ctypes.c_ulonglong, ctypes.c_uint, ctypes.c_uint, ctypes.c_longlong,
+                                 ctypes.c_longlong, ctypes.c_void_p]
     return lib
 
 
@@ -56,6 +58,25 @@ def test_philox_matches_library(rocrand_philox):
     rocrand_philox.pin_philox4x32_10(ctr.ctypes.data, key.ctypes.data, ref.ctypes.data, n)
     got = np.stack([O.philox(ctr[i], key[i]) for i in range(n)])
     assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("seed,t,stream,n0", [(7, 3, 2, 0), (0x123456789ABCDEF, 1, 0xFFFFFFFF, 5),
+                                               (4, 4294967295, 15, (1 << 34) + 3), (1, 20, 1023, 109_999_999)])
+def test_uniform_counter_layout_is_rocrand_subsequence(rocrand_philox, seed, t, stream, n0):
+    """The draw layout (element n of stream s at step t: word n&3 of the block
+    at counter {lo(n>>2), hi(n>>2), t, s}, key = seed) is rocRAND's Philox
+    generator seeded with `seed` at subsequence s * 2^32 + t and offset n:
+    a run of the oracle's draws equals that generator's successive outputs."""
+    length = 4099
+    ref = np.zeros(length, np.float32)
+    rocrand_philox.pin_uniforms(seed, t, stream, n0, length, ref.ctypes.data)
+    assert np.array_equal(O.uniforms(seed, t, stream, n0, length), ref)
+    # a swapped t / stream, or a neighbouring word, gives other draws
+    other = np.zeros(length, np.float32)
+    rocrand_philox.pin_uniforms(seed, stream, t, n0, length, other.ctypes.data)
+    assert (other != ref).mean() > 0.99 or t == stream
+    rocrand_philox.pin_uniforms(seed, t, stream, n0 + 1, length, other.ctypes.data)
+    assert np.array_equal(other[:-1], ref[1:])
 
 
 def test_uniforms_are_uniform_and_counter_based():
