@@ -536,9 +536,12 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
     // Codes are produced slot by slot and each code plane goes straight into
     // a ballot word, in message word order (4*chunk + slot)*bits + plane.
     // The scale, its reciprocal and the gate are wave-uniform and computed
-    // once per bucket.
+    // once per bucket.  x/s is formed as x * (1/s); a scale below 2^-126
+    // (whose reciprocal overflows) and x are first multiplied by 2^64, exact
+    // for both.  That case takes a wave-uniform branch, so the common one does
+    // no extra work per element.
     float sc = 0.0f, inv = 0.0f;
-    bool ok = true;
+    bool ok = true, tiny = false;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
@@ -546,7 +549,8 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
         if (ch == 0 || (cpb != 0 && (ch & (cpb - 1)) == 0)) {
             sc = uniform(s[ch]);
             ok = !gated || (sc > 0.0f && !isinf(sc));
-            inv = 1.0f / sc;
+            tiny = gated && sc < 0x1p-126f;
+            inv = 1.0f / (tiny ? sc * 0x1p64f : sc);
         }
         if (!ok) {
             // Zero or non-finite scale (uniform over the wave): the chunk is
@@ -569,13 +573,20 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
             r = philox10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), step, sid), k0, k1);
         }
         const uint32_t rr[4] = {r.x, r.y, r.z, r.w};
+        uint32_t cc[4];
+        if (tiny) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) cc[k] = code_of<QT>(q, comp(p[ch], k) * 0x1p64f, inv, rr[k]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) cc[k] = code_of<QT>(q, comp(p[ch], k), inv, rr[k]);
+        }
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const float x = comp(p[ch], k);
-            uint32_t cc = code_of<QT>(q, x, inv, rr[k]);
-            float dv = deq_of<QT>(q, lut, cc, x, sc);
+            float dv = deq_of<QT>(q, lut, cc[k], x, sc);
             if (!FULL && k >= nv) {
-                cc = 0u;
+                cc[k] = 0u;
                 dv = 0.0f;
             }
             set_comp(deq[ch], k, dv);
@@ -584,11 +595,11 @@ __device__ __forceinline__ void quantize_tile(const QDev& q, const float* lut, c
                     // Codes are below 2^bits, so the top plane is a compare.
 #pragma unroll
                     for (int pl = 0; pl < QT::bits(q); ++pl)
-                        sink.put(__builtin_amdgcn_ballot_w64(pl == QT::bits(q) - 1 ? cc >= (1u << pl)
-                                                                                    : ((cc >> pl) & 1u) != 0u));
+                        sink.put(__builtin_amdgcn_ballot_w64(pl == QT::bits(q) - 1 ? cc[k] >= (1u << pl)
+                                                                                    : ((cc[k] >> pl) & 1u) != 0u));
                 } else {
                     for (int pl = 0; pl < bits; ++pl)
-                        sink.put(__builtin_amdgcn_ballot_w64(((cc >> pl) & 1u) != 0u));
+                        sink.put(__builtin_amdgcn_ballot_w64(((cc[k] >> pl) & 1u) != 0u));
                 }
             }
         }
