@@ -1,9 +1,11 @@
 """Full-size parity: each workload at its real d and N through ea_step (the
-launch the benchmark times), checked against the oracle on sampled
-bucket-aligned segments.  Every step is bucket-local, so the oracle run on a
-segment (with its global element offset for the draws) is exactly the slice
-of a full run (pinned on the CPU by test_segment_equals_slice_of_full_run).
-Also: replaying steps from saved state is bit-identical (resume)."""
+launch the benchmark times), in both Adam placements and for the workload's
+step count, checked against the oracle on sampled bucket-aligned segments
+after every step.  Every step is bucket-local, so the oracle run on a segment
+(with its global element offset for the draws) is exactly the slice of a full
+run (pinned on the CPU by test_segment_equals_slice_of_full_run).  Also: the
+split calls give the fused call's bits, and replaying steps from saved state
+is bit-identical (resume)."""
 import numpy as np
 import pytest
 
@@ -18,7 +20,7 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 import paper_2205_14473_amd as E  # noqa: E402
 from paper_2205_14473_amd.state import allocate, init_state  # noqa: E402
-from parity_util import SPARSE_KINDS, Stats, _codes_match, _ulp_diff, close, configs, same_values  # noqa: E402
+from parity_util import SPARSE_KINDS, RoundCheck, Stats, configs  # noqa: E402
 
 
 def _segments(d, tile, count, seed):
@@ -28,12 +30,74 @@ def _segments(d, tile, count, seed):
     return [(k * tile, min(tile, d - k * tile)) for k in sorted(picks)]
 
 
-@pytest.mark.parametrize("key", ["bert", "resnet18", "resnet50", "gpt2m", "bert_topk", "bert_randk"])
-def test_full_size_sampled(key):
+class Sample:
+    """Bucket-aligned segments of the d-vector and device index tensors that
+    gather them (and their message words and scales) in one copy each."""
+
+    def __init__(self, oc, d, segs):
+        self.segs = segs
+        bw, bs = O.code_bits(oc.qw), O.code_bits(oc.qs)
+        Bw, Bs = O.bucket_len(oc.qw, d), O.bucket_len(oc.qs, d)
+        # one scale per bucket, or keep values per bucket for a sparsifier
+        per_w = oc.qw.keep if oc.qw.kind in SPARSE_KINDS else 1
+        per_s = oc.qs.keep if oc.qs.kind in SPARSE_KINDS else 1
+        sw = O.num_scales(oc.qw, d, d) > 0
+        ss = O.num_scales(oc.qs, d, d) > 0
+        el, ww, sc_w, wsd, sc_s = [], [], [], [], []
+        self.at = []
+        for n0, ln in segs:
+            e0, w0, s0, v0, t0 = (sum(len(a) for a in x) for x in (el, ww, sc_w, wsd, sc_s))
+            el.append(np.arange(n0, n0 + ln))
+            ww.append(np.arange(n0 // 256 * 4 * bw, n0 // 256 * 4 * bw + O.msg_words(oc.qw, ln)))
+            wsd.append(np.arange(n0 // 256 * 4 * bs, n0 // 256 * 4 * bs + O.msg_words(oc.qs, ln)))
+            nws, nss = O.num_scales(oc.qw, d, ln), O.num_scales(oc.qs, d, ln)
+            sc_w.append(np.arange(n0 // Bw * per_w, n0 // Bw * per_w + nws) if sw else np.zeros(0, np.int64))
+            sc_s.append(np.arange(n0 // Bs * per_s, n0 // Bs * per_s + nss) if ss else np.zeros(0, np.int64))
+            self.at.append(dict(e=slice(e0, e0 + ln), w=slice(w0, w0 + len(ww[-1])), s=slice(v0, v0 + len(wsd[-1])),
+                                sw=slice(s0, s0 + len(sc_w[-1])), ss=slice(t0, t0 + len(sc_s[-1]))))
+        dev = lambda a: torch.from_numpy(np.concatenate(a).astype(np.int64)).cuda()  # noqa: E731
+        self.el, self.ww, self.wsd, self.sc_w, self.sc_s = dev(el), dev(ww), dev(wsd), dev(sc_w), dev(sc_s)
+
+    def rows(self, t):
+        return None if t is None else t[:, self.el].cpu().numpy()
+
+    def vec(self, t):
+        return None if t is None else t[self.el].cpu().numpy()
+
+    def messages(self, rb):
+        i64 = torch.int64
+        return (rb.wcodes.view(i64)[:, self.ww].cpu().numpy().view(np.uint64),
+                rb.wscales[:, self.sc_w].cpu().numpy(),
+                rb.scodes.view(i64)[self.wsd].cpu().numpy().view(np.uint64),
+                rb.sscales[self.sc_s].cpu().numpy())
+
+    def put_back(self, rb, k, st):
+        """Reset the GPU state of segment k to the oracle's."""
+        idx = self.el[self.at[k]["e"]]
+        for name in ("e_w", "m_w", "v_w"):
+            if getattr(st, name) is not None:
+                getattr(rb, name)[:, idx] = torch.from_numpy(getattr(st, name)).cuda()
+        for name in ("e_s", "x", "m", "v"):
+            if getattr(st, name) is not None:
+                getattr(rb, name)[idx] = torch.from_numpy(getattr(st, name)).cuda()
+
+
+S, Wk = O.ADAM_AT_SERVER, O.ADAM_AT_WORKER
+FULL_CASES = [("bert", S, 100), ("bert", Wk, 100), ("resnet18", S, 50), ("resnet18", Wk, 50),
+              ("resnet50", S, 50), ("resnet50", Wk, 50), ("gpt2m", S, 10), ("gpt2m", Wk, 10),
+              ("bert_topk", S, 20), ("bert_topk", Wk, 20), ("bert_randk", S, 20)]
+
+
+@pytest.mark.parametrize("key,placement,T", FULL_CASES,
+                         ids=[f"{k}-{'server' if p == S else 'worker'}-{T}" for k, p, T in FULL_CASES])
+def test_full_size_sampled(key, placement, T):
+    """Each workload at its real d and N through ea_step, both placements,
+    for its step count (100 for the BERT-sized round): after every step the
+    sampled segments' messages and state equal the oracle's bit for bit."""
     w = W.WORKLOADS[key]
-    print(f"\n[fullsize] {w.name}", flush=True)
-    d, N, T = w.d, w.N, 3
-    oc, ec = configs(d, N, w.qw.fields(), w.qs.fields(), w.placement, w.seed, w.beta1, w.beta2, w.lr, w.eps)
+    d, N = w.d, w.N
+    print(f"\n[fullsize] {w.name} placement={placement} T={T}", flush=True)
+    oc, ec = configs(d, N, w.qw.fields(), w.qs.fields(), placement, w.seed, w.beta1, w.beta2, w.lr, w.eps)
     rb = allocate(ec)
     init_state(ec, rb)
     gen = torch.Generator(device="cuda")
@@ -41,53 +105,36 @@ def test_full_size_sampled(key):
     torch.randn(d, generator=gen, device="cuda", out=rb.x)
     rb.x.mul_(0.02)
     tile = max(O.bucket_len(oc.qw, d), O.bucket_len(oc.qs, d), 512)
-    segs = _segments(d, tile, 24, w.seed)
-    bw, bs = O.code_bits(oc.qw), O.code_bits(oc.qs)
-    Bw, Bs = O.bucket_len(oc.qw, d), O.bucket_len(oc.qs, d)
-    # per bucket: one scale, or keep values for a sparsifier (compared bit-exactly)
-    sp_w, sp_s = oc.qw.kind in SPARSE_KINDS, oc.qs.kind in SPARSE_KINDS
-    per_w, per_s = (oc.qw.keep if sp_w else 1), (oc.qs.keep if sp_s else 1)
-    x_host = rb.x.cpu().numpy()
-    states = {n0: O.State.init(oc, ln, x_host[n0:n0 + ln]) for n0, ln in segs}
+    smp = Sample(oc, d, _segments(d, tile, 24, w.seed))
+    x_host = smp.vec(rb.x)
+    states = [O.State.init(oc, ln, x_host[a["e"]]) for (n0, ln), a in zip(smp.segs, smp.at)]
     stats = Stats()
     for t in range(1, T + 1):
         W.device_gradients(w, t, rb.g)
-        g_host = {n0: rb.g[:, n0:n0 + ln].cpu().numpy() for n0, ln in segs}
+        g_host = smp.rows(rb.g)
         E.ea_step(ec, t, **rb.step_args())
         torch.cuda.synchronize()
-        wc, ws, sc, ss = rb.wcodes.cpu(), rb.wscales.cpu(), rb.scodes.cpu(), rb.sscales.cpu()
-        for n0, ln in segs:
-            st = states[n0]
-            out = O.step(oc, t, np.ascontiguousarray(g_host[n0]), st, n0=n0)
-            w0, w1 = n0 // 256 * 4 * bw, n0 // 256 * 4 * bw + out["wcodes"].shape[1]
-            v0, v1 = n0 // 256 * 4 * bs, n0 // 256 * 4 * bs + out["scodes"].shape[0]
-            ws_g = ws[:, n0 // Bw * per_w:n0 // Bw * per_w + out["wscales"].shape[1]].numpy()
-            ss_g = ss[n0 // Bs * per_s:n0 // Bs * per_s + out["sscales"].shape[0]].numpy()
-            assert same_values(ws_g, out["wscales"]) if sp_w else np.all(_ulp_diff(ws_g, out["wscales"]) <= 1)
-            assert same_values(ss_g, out["sscales"]) if sp_s else np.all(_ulp_diff(ss_g, out["sscales"]) <= 1)
-            ties = 0
-            for i in range(N):
-                ties += _codes_match(oc.qw, bw, d, n0, wc[i, w0:w1].numpy(), out["wcodes"][i],
-                                     None if sp_w else ws_g[i], None if sp_w else out["wscales"][i], stats,
-                                     f"worker {i} segment {n0}")
-            ties += _codes_match(oc.qs, bs, d, n0, sc[v0:v1].numpy(), out["scodes"], None if sp_s else ss_g,
-                                 None if sp_s else out["sscales"], stats, f"server segment {n0}")
-            stats.code_ties += ties
-            stats.code_entries += (N + 1) * ln
-            close("e_w", rb.e_w[:, n0:n0 + ln].cpu().numpy(), st.e_w, stats)
-            close("e_s", rb.e_s[n0:n0 + ln].cpu().numpy(), st.e_s, stats)
-            close("x", rb.x[n0:n0 + ln].cpu().numpy(), st.x, stats)
-            close("m", rb.m[n0:n0 + ln].cpu().numpy(), st.m, stats)
-            close("v", rb.v[n0:n0 + ln].cpu().numpy(), st.v, stats)
-            if ties or not np.array_equal(rb.x[n0:n0 + ln].cpu().numpy(), st.x):
-                stats.resyncs += 1     # put the oracle's segment state back on the GPU
-                rb.e_w[:, n0:n0 + ln].copy_(torch.from_numpy(st.e_w))
-                rb.e_s[n0:n0 + ln].copy_(torch.from_numpy(st.e_s))
-                rb.x[n0:n0 + ln].copy_(torch.from_numpy(st.x))
-                rb.m[n0:n0 + ln].copy_(torch.from_numpy(st.m))
-                rb.v[n0:n0 + ln].copy_(torch.from_numpy(st.v))
-    assert stats.code_ties <= 1e-6 * stats.code_entries + 1
-    print(f"[fullsize] {key}: {len(segs)} segments x {T} steps: {stats}", flush=True)
+        wc, ws, sc, ss = smp.messages(rb)
+        gpu = {k: smp.rows(getattr(rb, k)) for k in ("e_w", "m_w", "v_w")}
+        gpu.update({k: smp.vec(getattr(rb, k)) for k in ("e_s", "x", "m", "v")})
+        tied_round = False
+        for k, ((n0, ln), a) in enumerate(zip(smp.segs, smp.at)):
+            st = states[k]
+            out = O.step(oc, t, np.ascontiguousarray(g_host[:, a["e"]]), st, n0=n0, want_inputs=True)
+            chk = RoundCheck(oc, d, n0, t, out, stats, what=f"step {t} segment {n0}: ")
+            chk.messages(wc[:, a["w"]], ws[:, a["sw"]], sc[a["s"]], ss[a["ss"]])
+            seg = {name: (None if v is None else (v[:, a["e"]] if v.ndim == 2 else v[a["e"]]))
+                   for name, v in gpu.items()}
+            chk.state(seg, st)
+            if chk.tied:
+                tied_round = True
+                smp.put_back(rb, k, st)
+                stats.resyncs += 1
+        stats.tie_rounds += tied_round
+        stats.steps += 1
+    print(f"[fullsize] {key}: {len(smp.segs)} segments x {T} steps: {stats}", flush=True)
+    assert stats.tie_rounds == 0, f"{stats.scale_ties} validated one-ulp scale ties"
+    assert stats.code_ties == 0 and stats.resyncs == 0
     del rb
     torch.cuda.empty_cache()
 

@@ -200,10 +200,10 @@ EXTREME_KINDS = {
 @pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
 @pytest.mark.parametrize("kind", list(EXTREME_KINDS))
 def test_extreme_magnitudes(kind, placement):
-    """Buckets of subnormal gradients, of gradients near the binary32 maximum
-    (their squares, L2 norms and Adam second moments overflow to infinity), of
-    zeros, and mixed: both sides follow the same IEEE binary32 steps, so every
-    output still matches."""
+    """Buckets of subnormal gradients (with and without zeros), of gradients
+    near the binary32 maximum (their squares, L2 norms and Adam second moments
+    overflow to infinity), of zeros, and mixed: both sides follow the same IEEE
+    binary32 steps, so every output still matches."""
     import numpy as np
     d, N = 512 * 6 + 64, 4
     q = EXTREME_KINDS[kind]
@@ -215,8 +215,13 @@ def test_extreme_magnitudes(kind, placement):
         g[:, 0:512] = sgn[:, 0:512] * rng.uniform(1, 100, (N, 512)).astype(np.float32) * np.float32(1e-43)
         g[:, 512:1024] = sgn[:, 512:1024] * rng.uniform(0.5, 3.0, (N, 512)).astype(np.float32) * np.float32(1e38)
         g[:, 1536:2048] = sgn[:, 1536:2048] * np.float32(1e30)
-        g[:, 2048:] = (sgn[:, 2048:] * rng.standard_normal((N, d - 2048)).astype(np.float32)
-                       * np.exp(rng.uniform(-80, 80, (N, d - 2048))).astype(np.float32))
+        # subnormal values with zeros: a max-norm below 2^-126, whose reciprocal
+        # overflows, and zeros that must still quantize as zeros
+        k = rng.integers(-214, 215, (N, 512))
+        k[rng.random((N, 512)) < 0.4] = 0
+        g[:, 2048:2560] = (k.astype(np.float64) * 2.0 ** -149).astype(np.float32)
+        g[:, 2560:] = (sgn[:, 2560:] * rng.standard_normal((N, d - 2560)).astype(np.float32)
+                       * np.exp(rng.uniform(-80, 80, (N, d - 2560))).astype(np.float32))
         pair.step(t, g)
         # the float comparison cannot see NaN or infinite entries: require the
         # state bit for bit, NaN in the same places
@@ -225,6 +230,22 @@ def test_extreme_magnitudes(kind, placement):
             assert same_values(got, getattr(pair.ost, name)), f"step {t}: {name} differs"
         assert pair.stats.resyncs == 0
     pair.check_tie_budget()
+
+
+@pytest.mark.parametrize("kind", ["stoch2_max", "ex1"])
+def test_subnormal_learning_rate(kind):
+    """Adam at the workers with lr = 1e-40: every worker's update, hence the
+    message scales on both sides (max-norms), is subnormal; x/s is then formed
+    with the 2^64 pre-scale on both sides."""
+    d, N = 512 * 4 + 300, 4
+    q = EXTREME_KINDS[kind]
+    pair = Pair(d, N, q, q, O.ADAM_AT_WORKER, seed=12, lr=1e-40)
+    for t in range(1, 5):
+        g = _grads("student_t", 12, t, N, d)
+        g[:, 600:800] = 0.0
+        pair.step(t, g)
+    pair.check_tie_budget()
+    assert np.abs(pair.ost.x).max() > 0
 
 
 def test_full_precision_messages_unaligned():

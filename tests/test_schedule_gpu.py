@@ -16,7 +16,7 @@ if not torch.cuda.is_available():  # pragma: no cover - CPU-only host
     pytest.skip("needs a GPU", allow_module_level=True)
 
 import paper_2205_14473_amd as E  # noqa: E402
-from parity_util import Pair, close, configs, qfields, Stats  # noqa: E402
+from parity_util import Pair, Stats, close, configs, first_diff, qfields, same_values  # noqa: E402
 
 SIGN = lambda b, ef=1: qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, ef, b)  # noqa: E731
 STOCH = lambda bits, sc, b, ef=1: qfields(O.Q_STOCH_UNIFORM, bits, sc, ef, b)  # noqa: E731
@@ -76,8 +76,7 @@ def test_graph_replay_takes_the_next_step(case, sched):
 
 def test_run_many_steps_in_one_call():
     """One ea_run call over T rounds with a [T][N][d] gradient array, against
-    the oracle's T rounds (scaled sign: codes do not depend on the scale, so
-    the two trajectories stay comparable without resynchronization)."""
+    the oracle's T rounds: the state after the last round is bit-identical."""
     d, N, T = 2048 + 256, 4, 8
     sd = dict(kind=O.SCHED_STEP_DECAY, alpha=1e-3, factor=0.5, period=3)
     oc, ec = configs(d, N, SIGN(512), SIGN(512), O.ADAM_AT_SERVER, seed=5)
@@ -97,11 +96,10 @@ def test_run_many_steps_in_one_call():
     E.ea_run(ec, se, 1, T, g_dev, N * d, **args)
     torch.cuda.synchronize()
     stats = Stats()
-    close("x", rb.x.cpu().numpy(), st.x, stats)
-    close("m", rb.m.cpu().numpy(), st.m, stats)
-    close("v", rb.v.cpu().numpy(), st.v, stats)
-    close("e_s", rb.e_s.cpu().numpy(), st.e_s, stats)
-    close("e_w", rb.e_w.cpu().numpy(), st.e_w, stats)
+    for name in ("x", "m", "v", "e_s", "e_w"):
+        got, want = getattr(rb, name).cpu().numpy(), getattr(st, name)
+        assert same_values(got, want), f"{name} after {T} steps: {first_diff(got, want)}"
+        close(name, got, want, stats)
     # the messages left behind are the last round's
     words = E.ea_msg_words(ec.qs, d)
     assert np.array_equal(rb.scodes.cpu().numpy()[:words], out["scodes"])
