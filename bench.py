@@ -110,6 +110,20 @@ def stream_reference(rb, stream, reps=5):
             "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1)}
 
 
+def host_cpu():
+    """Model name of the host CPU and the logical CPUs this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0)), os.cpu_count()
+
+
 def cpu_baseline(E, w, cfg, rb, sample):
     """The oracle, as it stands, on the first `sample` parameters (one round)."""
     import numpy as np
@@ -127,9 +141,11 @@ def cpu_baseline(E, w, cfg, rb, sample):
     t0 = time.perf_counter()
     O.step(oc, 1, g, st, n0=0)
     dt = time.perf_counter() - t0
+    model, usable, total = host_cpu()
     return {"value": round(n / dt / 1e9, 6), "unit": "Gparam/s", "cores": 1, "kind": "oracle",
             "sample": f"one round over the first {n} of {cfg.d} parameters, N={cfg.N}, single thread, "
-                      f"{dt:.2f} s"}
+                      f"{dt:.2f} s",
+            "host_cpu": model, "nproc": usable, "cpu_count": total}
 
 
 def paper_toy(args, E, allocate, init_state):

@@ -1,10 +1,19 @@
-"""Build ``libea.so`` (the HIP kernels + C ABI) in-tree for gfx950 with hipcc.
+"""Build ``libea.so`` (the HIP kernels + C ABI) in-tree for gfx950.
 
 Flags that matter for results:
   -ffp-contract=off      every a*b+c stays two binary32 roundings (no FMA)
   (no fast-math)         binary32 division and square root are correctly rounded
   -packed-fp32-ops off   no packed FP32 instructions are generated
+
+Each source is compiled in two passes, as the HIP driver does internally: a
+device pass for gfx950, which alone gets the target feature that turns packed
+FP32 off, and a host pass that embeds the device pass's fat binary.  Both use
+one compilation-unit ID (it names file-scope device variables, which the host
+registers by name).  The objects are byte-identical to a one-command hipcc
+build with the same flags, and the host pass does not see a device feature it
+would warn about.
 """
+import hashlib
 import os
 import subprocess
 import sys
@@ -20,33 +29,45 @@ HEADERS = [os.path.join(CSRC, f) for f in ("ea_device.hpp", "ea_launch.hpp", "ea
     [os.path.join(ROOT, "include", "ea.h")]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+CLANG = os.environ.get("HIP_CLANG", "/opt/rocm/lib/llvm/bin/clang++")
 
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    "-x", "hip", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-ffp-contract=off", "-fno-fast-math",
-    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
+DEVICE_FLAGS = ["--cuda-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+
+def _run_all(cmds, verbose):
+    procs = []
+    for cmd in cmds:
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((cmd, subprocess.Popen(cmd)))
+    failed = [cmd for cmd, p in procs if p.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, failed[0])
 
 
 def build(verbose: bool = False, extra=()) -> str:
-    """Compile the library (always): each source to an object, in parallel,
-    then one link; returns its path."""
+    """Compile the library (always): the device passes of all sources in
+    parallel, then their host passes, then one link; returns its path."""
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
-    jobs = []
+    dev, host, objs = [], [], []
     for src in SOURCES:
-        obj = os.path.join(objdir, os.path.basename(src) + ".o")
-        cmd = [HIPCC, *FLAGS, *extra, "-c", src, "-o", obj]
-        if verbose:
-            print(" ".join(cmd), flush=True)
-        jobs.append((cmd, obj, subprocess.Popen(cmd)))
-    failed = [cmd for cmd, _, p in jobs if p.wait() != 0]
-    if failed:
-        raise subprocess.CalledProcessError(1, failed[0])
+        base = os.path.join(objdir, os.path.basename(src))
+        cuid = "-cuid=" + hashlib.sha256(os.path.basename(src).encode()).hexdigest()[:16]
+        dev.append([CLANG, *FLAGS, cuid, *extra, *DEVICE_FLAGS, src, "-o", base + ".hipfb"])
+        host.append([CLANG, *FLAGS, cuid, *extra, "--cuda-host-only", "-c", "-Xclang", "-fcuda-include-gpubinary",
+                     "-Xclang", base + ".hipfb", src, "-o", base + ".o"])
+        objs.append(base + ".o")
+    _run_all(dev, verbose)
+    _run_all(host, verbose)
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *[o for _, o, _ in jobs], "-o", tmp]
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

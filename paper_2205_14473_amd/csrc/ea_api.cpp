@@ -603,14 +603,16 @@ int ea_run(const ea_config_t* c, const ea_schedule_t* s, int64_t t0, int64_t ste
     if (g_step_stride < 0) return fail(EA_ERR_ARG, "g_step_stride must be >= 0");
     if ((rc = check_t(t0))) return rc;
     if (steps > 0 && (rc = check_t(t0 + steps - 1))) return rc;
-    // Validate every step's configuration before enqueueing any of them.
-    for (int64_t k = 0; k < steps; ++k) {
-        ea_config_t ck = *c;
-        schedule_values(s, c->lr, c->beta2, t0 + k, &ck.lr, &ck.beta2);
+    // Validate before enqueueing anything.  The steps' configurations differ
+    // from c only in lr and beta2, and a valid schedule keeps them valid at
+    // every step once they are at t0 (the step decay only shrinks a finite,
+    // non-negative alpha; the other schedules are constant in t), so one
+    // check covers the whole run.
+    if (steps > 0) {
+        ea_config_t c0 = *c;
+        schedule_values(s, c->lr, c->beta2, t0, &c0.lr, &c0.beta2);
         Plan p;
-        if ((rc = make_plan(&ck, &p))) return rc;
-        if (s->kind == EA_SCHED_CONSTANT) break;
-        if (s->kind == EA_SCHED_ASSUMPTION2) break;   // the same values at every step
+        if ((rc = make_plan(&c0, &p))) return rc;
     }
     for (int64_t k = 0; k < steps; ++k) {
         ea_config_t ck = *c;
