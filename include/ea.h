@@ -207,6 +207,25 @@ int ea_step(const ea_config_t *c, int64_t t, const float *g, float *e_w, float *
             float *m, float *v, float *e_s, float *x, uint64_t *wcodes, float *wscales,
             uint64_t *scodes, float *sscales, void *workspace, void *stream);
 
+/* ---- for callers that cannot allocate ------------------------------------ */
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): ea_step
+ * without the workspace argument.  The workspace that one-bucket quantizers
+ * need (ea_workspace_bytes) comes from a device array the library holds on
+ * each GPU it runs on, EA_NOALLOC_SCRATCH_BYTES bytes, until the process ends;
+ * the call itself allocates nothing (no hipMalloc, no allocating library
+ * routine).  Every call on one GPU shares that GPU's array: calls that overlap
+ * on one GPU (on different streams, or from different threads without
+ * ordering) race and give undefined results.  Nothing in the array needs to
+ * start at any value.  Returns EA_ERR_UNSUPPORTED, before any device work,
+ * when ea_workspace_bytes(c) exceeds EA_NOALLOC_SCRATCH_BYTES.  Other
+ * arguments, results and errors as ea_step. */
+#define EA_NOALLOC_SCRATCH_BYTES (16 << 20)
+int ea_step_noalloc(const ea_config_t *c, int64_t t, const float *g, float *e_w, float *m_w, float *v_w,
+                    float *m, float *v, float *e_s, float *x, uint64_t *wcodes, float *wscales,
+                    uint64_t *scodes, float *sscales, void *stream);
+
 /* ---- step-size schedules and multi-step calls ------------------------------ */
 
 /* lr_t and beta2_t (the paper's alpha_t and theta_t) at step t >= 1, in

@@ -17,6 +17,7 @@ EA_Q_NONE, EA_Q_SCALED_SIGN, EA_Q_STOCH_UNIFORM, EA_Q_DET_UNIFORM, EA_Q_POW2, EA
 EA_SCALE_L1, EA_SCALE_L2, EA_SCALE_MAX = 0, 1, 2
 EA_ADAM_AT_SERVER, EA_ADAM_AT_WORKER = 0, 1
 EA_SCHED_CONSTANT, EA_SCHED_ASSUMPTION2, EA_SCHED_STEP_DECAY = 0, 1, 2
+EA_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class Quant(C.Structure):
@@ -70,6 +71,7 @@ def _load():
         "ea_server_compress": (C.c_int, [CP, I64, P, P, P, P, P, P]),
         "ea_worker_apply": (C.c_int, [CP, P, P, P, P]),
         "ea_step": (C.c_int, [CP, I64] + [P] * 14),
+        "ea_step_noalloc": (C.c_int, [CP, I64] + [P] * 13),
         "ea_schedule_at": (C.c_int, [CP, SP, I64, P, P]),
         "ea_step_scheduled": (C.c_int, [CP, SP] + [P] * 15),
         "ea_run": (C.c_int, [CP, SP, I64, I64, P, I64] + [P] * 13),
@@ -192,6 +194,13 @@ def ea_step(cfg, t, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes, ssc
                               _stream(stream)))
 
 
+def ea_step_noalloc(cfg, t, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes, sscales, stream=None):
+    f, u = _f32(), _u64()
+    return _check(lib.ea_step_noalloc(C.byref(cfg), t, _ptr(g, f), _ptr(e_w, f), _ptr(m_w, f), _ptr(v_w, f),
+                                      _ptr(m, f), _ptr(v, f), _ptr(e_s, f), _ptr(x, f), _ptr(wcodes, u),
+                                      _ptr(wscales, f), _ptr(scodes, u), _ptr(sscales, f), _stream(stream)))
+
+
 def ea_schedule_at(cfg, sched, t):
     """(lr_t, beta2_t) of the schedule at step t, as Python floats of binary32 values."""
     lr, b2 = C.c_float(), C.c_float()
@@ -234,3 +243,4 @@ def ea_toy_grad(d, N, A, x_star, xi, x, g, grad_sq, workspace, stream=None):
     f = _f32()
     return _check(lib.ea_toy_grad(d, N, _ptr(A, f), _ptr(x_star, f), _ptr(xi, f), _ptr(x, f), _ptr(g, f),
                                   _ptr(grad_sq, torch.float64), _ptr(workspace), _stream(stream)))
+

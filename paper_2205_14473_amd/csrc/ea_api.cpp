@@ -7,10 +7,24 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "ea_launch.hpp"
 
 namespace {
+
+// Device memory of ea_step_noalloc: the workspace of a round with one-bucket
+// quantizers (per-tile partial norms and the server input), held by each GPU
+// the library runs on until the process ends.  Every kernel that uses it
+// writes each entry before reading it, so nothing needs clearing between
+// calls.  In host code the array's name is only a stand-in: its device
+// address, which differs per GPU, comes from scratch_ptr().
+constexpr int64_t kScratchBytes = EA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {nullptr};
 
 thread_local char g_err[512] = "";
 
@@ -373,6 +387,27 @@ int step_impl(const char* name, const ea_config_t* c, int64_t t, uint32_t* t_dev
     return hip_status(e, name);
 }
 
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+int scratch_ptr(void** out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(EA_ERR_HIP, "ea_step_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(EA_ERR_UNSUPPORTED, "ea_step_noalloc: device %d outside [0, %d)", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(EA_ERR_HIP, "ea_step_noalloc: hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return EA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -569,6 +604,23 @@ int ea_step(const ea_config_t* c, int64_t t, const float* g, float* e_w, float* 
 {
     return step_impl("ea_step", c, t, nullptr, nullptr, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales, scodes,
                      sscales, workspace, stream);
+}
+
+int ea_step_noalloc(const ea_config_t* c, int64_t t, const float* g, float* e_w, float* m_w, float* v_w, float* m,
+                    float* v, float* e_s, float* x, uint64_t* wcodes, float* wscales, uint64_t* scodes,
+                    float* sscales, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    if (p.ws_bytes > kScratchBytes)
+        return fail(EA_ERR_UNSUPPORTED, "ea_step_noalloc: this configuration needs %lld bytes of scratch memory, more "
+                    "than the %lld the library holds (EA_NOALLOC_SCRATCH_BYTES); use ea_step with a workspace",
+                    (long long)p.ws_bytes, (long long)kScratchBytes);
+    void* ws = nullptr;
+    if (p.ws_bytes > 0 && (rc = scratch_ptr(&ws))) return rc;
+    return step_impl("ea_step_noalloc", c, t, nullptr, nullptr, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales,
+                     scodes, sscales, ws, stream);
 }
 
 int ea_schedule_at(const ea_config_t* c, const ea_schedule_t* s, int64_t t, float* lr, float* beta2)

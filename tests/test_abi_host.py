@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(E):
     names = _declared()
-    assert len(names) == 18, names
+    assert len(names) == 19, names
     for n in names:
         assert hasattr(E.lib, n), f"{n} declared in include/ea.h but not exported"
 
@@ -213,3 +213,17 @@ def test_toy_grad_rejected_before_device_work(E):
     assert E.ea_toy_workspace_bytes(500) == 8 * (500 + 8)
     with pytest.raises(E.EAError):
         E.ea_toy_workspace_bytes(0)
+
+
+def test_noalloc_scratch_limit_matches_header_and_rejects_before_device_work(E):
+    src = open(os.path.join(ROOT, "include", "ea.h")).read()
+    m = re.search(r"#define EA_NOALLOC_SCRATCH_BYTES \((\d+) << (\d+)\)", src)
+    assert m and int(m.group(1)) << int(m.group(2)) == E.EA_NOALLOC_SCRATCH_BYTES
+    q = E.Quant(kind=1, scale=0, bits=1, error_feedback=1, bucket=0)
+    c = E.Config(d=8_000_000, N=4, placement=0, beta1=0.9, beta2=0.999, lr=1e-3, eps=1e-8, seed=1, qw=q, qs=q)
+    assert E.ea_workspace_bytes(c) > E.EA_NOALLOC_SCRATCH_BYTES
+    # fake device pointers: the call must fail on the size before it touches any
+    with pytest.raises(E.EAError) as ei:
+        E.ea_step_noalloc(c, 1, *([1 << 20] * 12), stream=0)
+    assert ei.value.code == E.EA_ERR_UNSUPPORTED and "scratch" in E.ea_last_error()
+
