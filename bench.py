@@ -150,11 +150,14 @@ def cpu_baseline(E, w, cfg, rb, sample):
 
 def paper_toy(args, E, allocate, init_state):
     """Section V-A on the device: per step, the N workers' gradients
-    2 A^T (A x - x* - xi_i) at the current x (ea_toy_grad), then one round
-    (Example 2 with k = -17, K = -11, Adam at the workers, beta = 0.9,
-    theta = 0.99, lr = 1e-4).  The noise draws of all steps are generated
-    before the timed region.  The problem lives in cache: the step is bound by
-    launch latency, so the roofline fraction is reported for completeness."""
+    2 A^T (A x - x* - xi_i) at the current x and one round (Example 2 with
+    k = -17, K = -11, Adam at the workers, beta = 0.9, theta = 0.99,
+    lr = 1e-4), plus ||grad F||^2 at x.  By default one ea_toy_step call (the
+    gradient producer fused into the round: two launches, the gradients never
+    leave the chip); --call split times ea_toy_grad followed by ea_step.  The
+    noise draws of all steps are generated before the timed region.  The
+    problem lives in cache and is bound by launch latency and the binary64
+    sums, so the roofline fraction is reported for completeness."""
     import torch
     toy = W.PAPER_TOY
     d, N = toy["d"], toy["N"]
@@ -173,10 +176,15 @@ def paper_toy(args, E, allocate, init_state):
     ws = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
     step_args = rb.step_args()
+    fused = args.call != "split"
 
     def one(k):
-        E.ea_toy_grad(d, N, A, xs, xi[k], rb.x, rb.g, gsq[k:k + 1], ws, stream=stream)
-        E.ea_step(cfg, k + 1, **step_args, stream=stream)
+        if fused:
+            E.ea_toy_step(cfg, k + 1, A, xs, xi[k], rb.e_w, rb.m_w, rb.v_w, rb.m, rb.v, rb.e_s, rb.x, rb.wcodes,
+                          rb.scodes, gsq[k:k + 1], None, ws, stream=stream)
+        else:
+            E.ea_toy_grad(d, N, A, xs, xi[k], rb.x, rb.g, gsq[k:k + 1], ws, stream=stream)
+            E.ea_step(cfg, k + 1, **step_args, stream=stream)
 
     for k in range(args.warmup):
         one(k)
@@ -188,17 +196,21 @@ def paper_toy(args, E, allocate, init_state):
     stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
-    alg = algorithmic_bytes(E, cfg) + 2 * 4 * d * d      # the round + A read twice by the gradient
+    alg = algorithmic_bytes(E, cfg) + 4 * d * d      # the round + A read once by the gradient producer
+    if not fused:
+        alg += 4 * d * d + 2 * 4 * N * d             # A read again, g written and read back
     g = gsq.cpu().numpy()
     line = {
         "metric": "Section V-A toy problem, steps per second (gradient producer + round)",
         "value": round(1e3 / ms, 1), "unit": "steps/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
-        "config": {"workload": "paper_toy d=500 N=10 Example 2, Adam at the workers", "d": d, "N": N},
+        "config": {"workload": "paper_toy d=500 N=10 Example 2, Adam at the workers", "d": d, "N": N,
+                   "call": "ea_toy_step" if fused else "ea_toy_grad + ea_step"},
         "roofline": {"bound": "hbm", "achieved": round(alg / (ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(alg / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 5), "traffic": None,
-                     "kernel": "toy gradient kernels + step_kernel (cache-resident; launch-bound)"},
+                     "kernel": ("toy residual + toy_round_kernel" if fused else "toy gradient kernels + step_kernel")
+                     + " (cache-resident; launch-bound)"},
         "grad_sq_first_last": [float(g[0]), float(g[-1])],
     }
     print(json.dumps(line), flush=True)

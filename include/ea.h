@@ -281,7 +281,7 @@ int ea_run(const ea_config_t *c, const ea_schedule_t *s, int64_t t0, int64_t ste
 
 /* ---- the toy problem of Section V-A -------------------------------------- */
 
-/* Device workspace (bytes) of ea_toy_grad for dimension d. */
+/* Device workspace (bytes) of ea_toy_grad and ea_toy_step for dimension d. */
 int64_t ea_toy_workspace_bytes(int64_t d);
 
 /* Gradients of f(x) = E_xi || A x - (x* + xi) ||^2 (Section V-A) for N
@@ -295,6 +295,26 @@ int64_t ea_toy_workspace_bytes(int64_t d);
  *   1 <= d <= 65536, 1 <= N <= 1024. */
 int ea_toy_grad(int64_t d, int32_t N, const float *A, const float *x_star, const float *xi, const float *x,
                 float *g, double *grad_sq, void *workspace, void *stream);
+
+/* One round of the toy problem of Section V-A with the workers' gradients
+ * formed inside it (Figure 1's setting): g_i = 2 A^T (A x - x* - xi_i) at the
+ * current x, then the round of ea_step on those gradients, and, if grad_sq
+ * is not NULL, the squared norm of the full gradient 2 A^T (A x - x*) at that
+ * x (Figure 1's y-axis).  The gradients are not written to memory unless
+ * g_out is given.  Both quantizers must be without scales (EA_Q_POW2,
+ * Example 2; EA_Q_NONE), else EA_ERR_UNSUPPORTED: the message of a scaled
+ * quantizer would need the whole bucket's gradient first.
+ *   A (device, d*d, row-major), x_star (device, d), xi (device, N*d: the
+ *   workers' noise draws for this step), e_w, m_w, v_w, m, v, e_s, x, wcodes,
+ *   scodes as ea_step (no scales); grad_sq (device, one double, write, or
+ *   NULL); g_out (device, N*d, write, or NULL); workspace (device,
+ *   ea_toy_workspace_bytes(d) bytes, 8-byte aligned).
+ *   The gradients' products are summed in binary64 (in another order than
+ *   ea_toy_grad's, with fused multiply-adds) and each g_i rounded once to
+ *   binary32.  1 <= d <= 65536, 1 <= N <= 1024, 1 <= t <= 2^32-1. */
+int ea_toy_step(const ea_config_t *c, int64_t t, const float *A, const float *x_star, const float *xi, float *e_w,
+                float *m_w, float *v_w, float *m, float *v, float *e_s, float *x, uint64_t *wcodes,
+                uint64_t *scodes, double *grad_sq, float *g_out, void *workspace, void *stream);
 
 #ifdef __cplusplus
 }

@@ -17,7 +17,7 @@ _EXPORTS = (
     "ea_code_bits", "ea_msg_words", "ea_msg_scales", "ea_msg_bits", "ea_workspace_bytes", "ea_validate",
     "ea_last_error", "ea_state_init", "ea_worker_compress", "ea_server_aggregate_adam", "ea_server_compress",
     "ea_worker_apply", "ea_step", "ea_step_noalloc", "ea_schedule_at", "ea_step_scheduled", "ea_run", "ea_toy_workspace_bytes",
-    "ea_toy_grad",
+    "ea_toy_grad", "ea_toy_step",
 )
 __all__ = list(_EXPORTS)
 

@@ -77,6 +77,7 @@ def _load():
         "ea_run": (C.c_int, [CP, SP, I64, I64, P, I64] + [P] * 13),
         "ea_toy_workspace_bytes": (I64, [I64]),
         "ea_toy_grad": (C.c_int, [I64, I32] + [P] * 8),
+        "ea_toy_step": (C.c_int, [CP, I64] + [P] * 16),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -244,3 +245,12 @@ def ea_toy_grad(d, N, A, x_star, xi, x, g, grad_sq, workspace, stream=None):
     return _check(lib.ea_toy_grad(d, N, _ptr(A, f), _ptr(x_star, f), _ptr(xi, f), _ptr(x, f), _ptr(g, f),
                                   _ptr(grad_sq, torch.float64), _ptr(workspace), _stream(stream)))
 
+
+def ea_toy_step(cfg, t, A, x_star, xi, e_w, m_w, v_w, m, v, e_s, x, wcodes, scodes, grad_sq, g_out, workspace,
+                stream=None):
+    import torch
+    f, u = _f32(), _u64()
+    return _check(lib.ea_toy_step(C.byref(cfg), t, _ptr(A, f), _ptr(x_star, f), _ptr(xi, f), _ptr(e_w, f),
+                                  _ptr(m_w, f), _ptr(v_w, f), _ptr(m, f), _ptr(v, f), _ptr(e_s, f), _ptr(x, f),
+                                  _ptr(wcodes, u), _ptr(scodes, u), _ptr(grad_sq, torch.float64), _ptr(g_out, f),
+                                  _ptr(workspace), _stream(stream)))

@@ -702,4 +702,50 @@ int ea_toy_grad(int64_t d, int32_t N, const float* A, const float* x_star, const
                       "ea_toy_grad");
 }
 
+int ea_toy_step(const ea_config_t* c, int64_t t, const float* A, const float* x_star, const float* xi, float* e_w,
+                float* m_w, float* v_w, float* m, float* v, float* e_s, float* x, uint64_t* wcodes, uint64_t* scodes,
+                double* grad_sq, float* g_out, void* workspace, void* stream)
+{
+    Plan p;
+    int rc = make_plan(c, &p);
+    if (rc) return rc;
+    if ((rc = check_t(t))) return rc;
+    if (c->d > ea::kToyMaxD)
+        return fail(EA_ERR_ARG, "ea_toy_step needs d <= %lld (got %lld)", (long long)ea::kToyMaxD, (long long)c->d);
+    const auto scaleless = [](int32_t k) { return k == EA_Q_POW2 || k == EA_Q_NONE; };
+    if (!scaleless(c->qw.kind) || !scaleless(c->qs.kind))
+        return fail(EA_ERR_UNSUPPORTED, "ea_toy_step: both quantizers must be without scales (EA_Q_POW2 or EA_Q_NONE); "
+                    "use ea_toy_grad and ea_step for the others");
+    const bool srv = c->placement == EA_ADAM_AT_SERVER;
+    PtrCheck pc;
+    pc.need(A, true, 4, "A");
+    pc.need(x_star, true, 4, "x_star");
+    pc.need(xi, true, 4, "xi");
+    pc.need(e_w, true, 4, "e_w");
+    pc.need(m_w, !srv, 4, "m_w");
+    pc.need(v_w, !srv, 4, "v_w");
+    pc.need(m, srv, 4, "m");
+    pc.need(v, srv, 4, "v");
+    pc.need(e_s, true, 4, "e_s");
+    pc.need(x, true, 4, "x");
+    pc.need(wcodes, true, 8, "wcodes");
+    pc.need(scodes, true, 8, "scodes");
+    pc.need(grad_sq, false, 8, "grad_sq");
+    pc.need(g_out, false, 4, "g_out");
+    pc.need(workspace, true, 8, "workspace");
+    if (pc.rc) return pc.rc;
+    ea::StepArgs a = base_args(c, p, t);
+    a.e_w = e_w;
+    a.m_w = srv ? nullptr : m_w;
+    a.v_w = srv ? nullptr : v_w;
+    a.m = srv ? m : nullptr;
+    a.v = srv ? v : nullptr;
+    a.e_s = e_s;
+    a.x = x;
+    a.wcodes = wcodes;
+    a.scodes = scodes;
+    return hip_status(ea::launch_toy_step(a, A, x_star, xi, grad_sq, g_out, workspace, (hipStream_t)stream),
+                      "ea_toy_step");
+}
+
 }  // extern "C"

@@ -101,5 +101,10 @@ constexpr int64_t kToyMaxD = 65536;
 int64_t toy_workspace_bytes(int64_t d);
 hipError_t launch_toy_grad(int64_t d, int32_t N, const float* A, const float* xs, const float* xi, const float* x,
                            float* g, double* grad_sq, void* workspace, hipStream_t s);
+// One round of the toy problem with the gradients formed inside it (the
+// quantizers have no scales); `a` carries the configuration, the state and
+// the messages.  g_out (nullable) receives the workers' gradients.
+hipError_t launch_toy_step(const StepArgs& a, const float* A, const float* xs, const float* xi, double* grad_sq,
+                           float* g_out, void* workspace, hipStream_t s);
 
 }  // namespace ea

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported(E):
     names = _declared()
-    assert len(names) == 19, names
+    assert len(names) == 20, names
     for n in names:
         assert hasattr(E.lib, n), f"{n} declared in include/ea.h but not exported"
 
@@ -210,7 +210,7 @@ def test_toy_grad_rejected_before_device_work(E):
     assert E.lib.ea_toy_grad(500, 10, *p, P(4100), ws, None) == E.EA_ERR_ALIGN
     assert E.lib.ea_toy_grad(500, 10, *p, None, None, None) == E.EA_ERR_ARG
     assert E.lib.ea_toy_grad(500, 10, *p, None, P(4100), None) == E.EA_ERR_ALIGN
-    assert E.ea_toy_workspace_bytes(500) == 8 * (500 + 8)
+    assert E.ea_toy_workspace_bytes(500) == 8 * (500 + 8 + 1)     # r, per-block norms, counter
     with pytest.raises(E.EAError):
         E.ea_toy_workspace_bytes(0)
 
@@ -227,3 +227,15 @@ def test_noalloc_scratch_limit_matches_header_and_rejects_before_device_work(E):
         E.ea_step_noalloc(c, 1, *([1 << 20] * 12), stream=0)
     assert ei.value.code == E.EA_ERR_UNSUPPORTED and "scratch" in E.ea_last_error()
 
+
+def test_toy_step_rejects_scaled_quantizers_before_device_work(E):
+    q = E.Quant(kind=3, bits=2, error_feedback=1, bucket=0)      # Example 1: one max-norm scale
+    c = E.Config(d=500, N=10, placement=1, beta1=0.9, beta2=0.99, lr=1e-4, eps=1e-8, seed=1, qw=q, qs=q)
+    with pytest.raises(E.EAError) as ei:
+        E.ea_toy_step(c, 1, *([1 << 20] * 15), stream=0)
+    assert ei.value.code == E.EA_ERR_UNSUPPORTED
+    q2 = E.Quant(kind=4, error_feedback=1, pow2_kmin=-17, pow2_kmax=-11)
+    c2 = E.Config(d=70000, N=10, placement=1, beta1=0.9, beta2=0.99, lr=1e-4, eps=1e-8, seed=1, qw=q2, qs=q2)
+    with pytest.raises(E.EAError) as ei:
+        E.ea_toy_step(c2, 1, *([1 << 20] * 15), stream=0)
+    assert ei.value.code == E.EA_ERR_ARG

@@ -100,3 +100,97 @@ def test_figure1_setting_on_device(example):
     assert norms[-1] < norms[0]
     print(f"\n[toy] figure-1 setting {example}: |grad F|^2 {norms[0]:.4g} -> {norms[-1]:.4g}; {pair.stats}",
           flush=True)
+
+
+# ---------------------------------------------------------------------------
+# ea_toy_step: the gradient producer fused into the round.
+# ---------------------------------------------------------------------------
+from paper_2205_14473_amd.state import allocate, init_state  # noqa: E402
+from parity_util import RoundCheck, Stats, configs  # noqa: E402
+
+EX2 = qfields(O.Q_POW2, kmin=-17, kmax=-11)
+NONE = qfields(O.Q_NONE)
+FUSED = [(500, 10, EX2, O.ADAM_AT_WORKER), (500, 10, NONE, O.ADAM_AT_SERVER), (500, 10, EX2, O.ADAM_AT_SERVER),
+         (64, 3, EX2, O.ADAM_AT_SERVER), (65, 1, EX2, O.ADAM_AT_WORKER), (1000, 17, EX2, O.ADAM_AT_WORKER),
+         (777, 31, NONE, O.ADAM_AT_WORKER), (3000, 4, EX2, O.ADAM_AT_SERVER), (1, 2, EX2, O.ADAM_AT_WORKER),
+         (300, 15, EX2, O.ADAM_AT_WORKER), (300, 16, NONE, O.ADAM_AT_SERVER)]
+
+
+def _ulps(a, b):
+    ai = np.asarray(a, np.float32).view(np.int32).astype(np.int64)
+    bi = np.asarray(b, np.float32).view(np.int32).astype(np.int64)
+    ai = np.where(ai < 0, -(ai & 0x7FFFFFFF), ai)
+    bi = np.where(bi < 0, -(bi & 0x7FFFFFFF), bi)
+    return np.abs(ai - bi)
+
+
+@pytest.mark.parametrize("d,N,q,placement", FUSED,
+                         ids=[f"d{d}-N{N}-{'ex2' if q['kind'] == O.Q_POW2 else 'full'}-"
+                              f"{'worker' if p == O.ADAM_AT_WORKER else 'server'}" for d, N, q, p in FUSED])
+def test_toy_step_equals_gradient_then_round(d, N, q, placement):
+    """Each step: the fused call's gradients (read back through g_out) equal
+    the oracle's toy gradient at the same x to the last place (binary64 sums
+    in another order), its squared norm to 1e-12, and the round on those
+    gradients equals the oracle's round on them bit for bit."""
+    rng = np.random.default_rng(d * 131 + N)
+    A = rng.standard_normal((d, d)).astype(np.float32)
+    xs = (rng.standard_normal(d) * math.sqrt(0.1)).astype(np.float32)
+    x1 = (rng.standard_normal(d) * 0.01).astype(np.float32)
+    lr = 1e-4 if q["kind"] == O.Q_POW2 else 1e-3
+    oc, ec = configs(d, N, q, q, placement, seed=9, beta1=0.9, beta2=0.99, lr=lr)
+    rb = allocate(ec)
+    init_state(ec, rb)
+    rb.x.copy_(torch.from_numpy(x1))
+    st = O.State.init(oc, d, x1)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    A_d, xs_d = dev(A), dev(xs)
+    g_d = torch.empty((N, d), dtype=torch.float32, device="cuda")
+    gs_d = torch.zeros(1, dtype=torch.float64, device="cuda")
+    ws = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+    stats = Stats()
+    worst = 0
+    for t in range(1, 7):
+        xi = (rng.standard_normal((N, d)) * math.sqrt(0.1)).astype(np.float32)
+        E.ea_toy_step(ec, t, A_d, xs_d, dev(xi), rb.e_w, rb.m_w, rb.v_w, rb.m, rb.v, rb.e_s, rb.x, rb.wcodes,
+                      rb.scodes, gs_d, g_d, ws)
+        torch.cuda.synchronize()
+        g = g_d.cpu().numpy()
+        go, gso = O.toy_grad(A, xs, xi, st.x)
+        u = _ulps(g, go)
+        worst = max(worst, int(u.max()))
+        assert u.max() <= 1, f"step {t}: gradient differs from the oracle's by {u.max()} ulps"
+        assert float(gs_d.item()) == pytest.approx(gso, rel=1e-12)
+        out = O.step(oc, t, g, st, want_inputs=True)
+        chk = RoundCheck(oc, d, 0, t, out, stats, what=f"step {t}: ")
+        none = np.zeros((N, 0), np.float32)
+        chk.messages(rb.wcodes.cpu().numpy(), none, rb.scodes.cpu().numpy(), none[0])
+        host = lambda a: None if a is None else a.cpu().numpy()  # noqa: E731
+        chk.state({k: host(getattr(rb, k)) for k in ("e_w", "e_s", "x", "m", "v", "m_w", "v_w")}, st)
+        assert not chk.tied
+        stats.steps += 1
+    print(f"\n[toy step] d={d} N={N}: gradients within {worst} ulp; rounds bit-exact; {stats}", flush=True)
+
+
+def test_toy_step_optional_outputs_change_nothing():
+    """Without g_out and grad_sq the fused call leaves the same bits."""
+    d, N = 500, 10
+    rng = np.random.default_rng(5)
+    A = torch.from_numpy(rng.standard_normal((d, d)).astype(np.float32)).cuda()
+    xs = torch.from_numpy((rng.standard_normal(d) * 0.3).astype(np.float32)).cuda()
+    _, ec = configs(d, N, EX2, EX2, O.ADAM_AT_WORKER, seed=9, beta1=0.9, beta2=0.99, lr=1e-4)
+    a, b = allocate(ec), allocate(ec)
+    for rb in (a, b):
+        init_state(ec, rb)
+        rb.x.zero_()
+    ws_a = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty_like(ws_a)
+    g = torch.empty((N, d), dtype=torch.float32, device="cuda")
+    gs = torch.zeros(1, dtype=torch.float64, device="cuda")
+    for t in range(1, 5):
+        xi = torch.from_numpy((rng.standard_normal((N, d)) * 0.3).astype(np.float32)).cuda()
+        E.ea_toy_step(ec, t, A, xs, xi, a.e_w, a.m_w, a.v_w, a.m, a.v, a.e_s, a.x, a.wcodes, a.scodes, gs, g, ws_a)
+        E.ea_toy_step(ec, t, A, xs, xi, b.e_w, b.m_w, b.v_w, b.m, b.v, b.e_s, b.x, b.wcodes, b.scodes, None, None,
+                      ws_b)
+    torch.cuda.synchronize()
+    for k in ("e_w", "m_w", "v_w", "e_s", "x", "wcodes", "scodes"):
+        assert torch.equal(getattr(a, k).view(torch.uint8), getattr(b, k).view(torch.uint8)), k
