@@ -125,13 +125,21 @@ struct Special {
     void (*kernel)(StepArgs);   // whole tiles
     void (*edge)(StepArgs);     // the ragged last tile
     int tiles;                  // tiles per block of `kernel`
+    void (*many)(StepArgs);     // whole tiles with more workers than waves
 };
+
+// Waves per SIMD of the kernels for more workers than waves: the next
+// group's rows and the sums are live together.
+#ifndef EA_PIPE_MIN_WAVES
+#define EA_PIPE_MIN_WAVES 4
+#endif
 
 #define EA_SPECIAL(CC, QWT, QST, PLC)                                                               \
     Special{CC, QWT::kind(QDev{}), QWT::bits(QDev{}), QWT::norm(QDev{}), QWT::cpb(QDev{}),         \
             QST::kind(QDev{}), QST::bits(QDev{}), QST::norm(QDev{}), QST::cpb(QDev{}), PLC,         \
             step_kernel<CC, true, true, QWT, QST, PLC>, step_kernel<CC, true, false, QWT, QST, PLC>,         \
-            round_tiles_per_block(CC, PLC == AT_SERVER)}
+            round_tiles_per_block(CC, PLC == AT_SERVER),                                               \
+            step_kernel<CC, true, true, QWT, QST, PLC, EA_PIPE_MIN_WAVES, true>}
 
 const Special kSpecials[] = {
     EA_SPECIAL(2, Stoch4L2Q2, Stoch4L2Q2, AT_SERVER),
@@ -220,7 +228,7 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
         const dim3 grid((unsigned)((nfull + K - 1) / K)), block((unsigned)(G * kWave));
         const size_t lds = round_lds_bytes(a.N, C, G, K);
         if (sp) {
-            hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
+            hipLaunchKernelGGL(a.N > G ? sp->many : sp->kernel, grid, block, lds, s, b);
         } else if (sk) {
             hipLaunchKernelGGL(sk->kernel, grid, block, lds, s, b);
         } else if (hk) {

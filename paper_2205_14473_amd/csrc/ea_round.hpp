@@ -1152,18 +1152,25 @@ __device__ __forceinline__ TilePos tile_at(const StepArgs& a, int64_t tile)
     return t;
 }
 
-// Worker i on the block's nt consecutive tiles: the rows of all of them are
-// loaded first, so the later tiles' loads are in flight while the first is
-// compressed; the codes of the tiles leave through one sink, as one piece.
-// Tile k's dequantized values go to slots + (k*G + w)*C*64.
-template <int C, int K, bool VEC, bool FULL, class QW, int PL>
-__device__ __forceinline__ void worker_tiles(const StepArgs& a, const TilePos (&tp)[K], int nt, const float* lut_w,
-                                             int i, float4* slots, int G, int w)
+// Worker i's rows of the block's nt consecutive tiles.
+template <int C, int K, bool VEC, bool FULL, int PL>
+__device__ __forceinline__ void worker_rows(const StepArgs& a, const TilePos (&tp)[K], int nt, int i,
+                                            WorkerRows<C> (&r)[K])
 {
-    WorkerRows<C> r[K];
 #pragma unroll
     for (int k = 0; k < K; ++k)
         if (k < nt) worker_load<C, VEC, FULL, PL>(a, tp[k], i, r[k]);
+}
+
+// Worker i on the block's nt consecutive tiles, from rows loaded beforehand
+// (worker_rows; all tiles' rows are loaded first, so the later tiles' loads
+// are in flight while the first is compressed); the codes of the tiles leave
+// through one sink, as one piece.  Tile k's dequantized values go to
+// slots + (k*G + w)*C*64.
+template <int C, int K, bool VEC, bool FULL, class QW, int PL>
+__device__ __forceinline__ void worker_tiles(const StepArgs& a, const TilePos (&tp)[K], int nt, const float* lut_w,
+                                             int i, WorkerRows<C> (&r)[K], float4* slots, int G, int w)
+{
     WordSink sink = message_sink<QW>(a.qw, a.wcodes + (int64_t)i * a.qw.words, tp[0].base);
 #pragma unroll
     for (int k = 0; k < K; ++k)
@@ -1171,6 +1178,16 @@ __device__ __forceinline__ void worker_tiles(const StepArgs& a, const TilePos (&
             worker_compute<C, VEC, FULL, QW, PL>(a, tp[k], lut_w, i, r[k], sink,
                                                  slots + ((int64_t)k * G + w) * C * kWave);
     sink.flush();
+}
+
+// Worker i on the block's tiles: its rows are loaded, then compressed.
+template <int C, int K, bool VEC, bool FULL, class QW, int PL>
+__device__ __forceinline__ void worker_round(const StepArgs& a, const TilePos (&tp)[K], int nt, const float* lut_w,
+                                             int i, float4* slots, int G, int w)
+{
+    WorkerRows<C> r[K];
+    worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, i, r);
+    worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, i, r, slots, G, w);
 }
 
 // ---------------------------------------------------------------------------
@@ -1190,7 +1207,7 @@ __device__ __forceinline__ void worker_tiles(const StepArgs& a, const TilePos (&
 // the wait for the workers, without the loaded rows being live during the
 // earlier groups.
 // ---------------------------------------------------------------------------
-template <int C, int K, bool VEC, bool FULL, class QW, class QS, int PL>
+template <int C, int K, bool VEC, bool FULL, class QW, class QS, int PL, bool PIPE>
 __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, int nt, const float* lut_w,
                                             const float* lut_s, float4* xfer, int G)
 {
@@ -1206,17 +1223,39 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
 
-    // Handoff layout: [group buffer][tile][wave][chunk][lane].
+    // Handoff layout: [group buffer][tile][wave][chunk][lane].  With more
+    // workers than waves, PIPE kernels load a wave's next worker's rows as
+    // soon as it has handed its current worker over, so that they arrive
+    // during the barrier and the gather rather than after them (the rows and
+    // the sums are then live together, which costs registers).
     const int64_t per_buf = (int64_t)K * G * C * kWave;
     int buf = 0, g0 = 0;
-    for (; g0 + G < a.N; g0 += G, buf ^= 1) {
-        float4* slots = xfer + buf * per_buf;
-        worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
-        __syncthreads();
-        if (w < nt) gather_group<C>(slots + (int64_t)w * G * C * kWave, G, acc);
+    float4* slots;
+    if constexpr (PIPE) {
+        WorkerRows<C> rows[K];
+        if (w < a.N) worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, w, rows);
+        for (; g0 + G < a.N; g0 += G, buf ^= 1) {
+            slots = xfer + buf * per_buf;
+            worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, rows, slots, G, w);
+            if (g0 + G + w < a.N) worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, g0 + G + w, rows);
+            __syncthreads();
+            if (w < nt) gather_group<C>(slots + (int64_t)w * G * C * kWave, G, acc);
+        }
+        slots = xfer + buf * per_buf;
+        if (g0 + w < a.N) {
+            if (g0 == 0) worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, w, rows);
+            worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, rows, slots, G, w);
+        }
+    } else {
+        for (; g0 + G < a.N; g0 += G, buf ^= 1) {
+            slots = xfer + buf * per_buf;
+            worker_round<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
+            __syncthreads();
+            if (w < nt) gather_group<C>(slots + (int64_t)w * G * C * kWave, G, acc);
+        }
+        slots = xfer + buf * per_buf;
+        if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
     }
-    float4* slots = xfer + buf * per_buf;
-    if (g0 + w < a.N) worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
     const TilePos t = tile_at<C>(a, tile0 + (w < nt ? w : 0));
     ServerRows<C> sr;
     if (w < nt) load_server<C, VEC, FULL, PL>(a, t.base, t.nch, true, !sglobal, sr);
@@ -1440,13 +1479,14 @@ inline int round_waves(int N, int C, int K, size_t lds_limit, int placement)
 // the server input, which it leaves in ubuf with per-tile partial norms.
 //
 // MW > 0 overrides the minimum waves per SIMD of the launch bounds (the
-// register cap).
+// register cap).  PIPE: the variant for more workers than waves, which loads
+// each wave's next worker while the block gathers the current group.
 //
 // FULL kernels (rows 16-byte aligned) take the tiles that lie wholly inside d
 // and carry no bounds checks; the others take any tile.  A launch covers
 // tiles [a.tile0, a.tile1); block b works on the K tiles from
 // a.tile0 + b*K.
-template <int C, bool VEC, bool FULL, class QW, class QS, int PL, int MW = 0>
+template <int C, bool VEC, bool FULL, class QW, class QS, int PL, int MW = 0, bool PIPE = false>
 __global__ __launch_bounds__(max_round_waves(C) * kWave,
                              MW > 0 ? MW : round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
     StepArgs args)
@@ -1474,7 +1514,7 @@ __global__ __launch_bounds__(max_round_waves(C) * kWave,
     constexpr int K = kernel_tiles(C, FULL, PL, half_kernel<QW, QS, PL>());
     const int64_t first = a.tile0 + (int64_t)blockIdx.x * K;
     const int64_t left = a.tile1 - first;
-    round_tiles<C, K, VEC, FULL, QW, QS, PL>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G);
+    round_tiles<C, K, VEC, FULL, QW, QS, PL, PIPE>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G);
 }
 
 }  // namespace
