@@ -17,7 +17,7 @@ constexpr HalfKernel half()
 {
     return HalfKernel{1, QW::kind(QDev{}), QW::bits(QDev{}), QW::norm(QDev{}), QW::cpb(QDev{}),
                       step_kernel<1, true, true, QW, QRt, -1>, kernel_tiles(1, true, -1, true),
-                      worker_kernel<1, true, QW>, aggregate_kernel<1, true, QW>,
+                      worker_kernel<1, true, QW>, aggregate_kernel<1, true, QW>, aggregate_kernel<1, true, QW, true>,
                       server_kernel<1, true, QW>, apply_kernel<1, true, QW>};
 }
 

@@ -64,6 +64,7 @@ struct HalfKernel {
     int tiles;                // tiles per block
     void (*worker)(StepArgs);     // split call: one worker's compression (aligned rows)
     void (*aggregate)(StepArgs);  // split call: decode and average of the N messages
+    void (*aggregate_full)(StepArgs);  // the same on tiles that lie wholly inside d
     // The same quantizer on the server side of the split calls (aligned rows):
     void (*server)(StepArgs);     // the server's compression
     void (*apply)(StepArgs);      // x -= the server message

@@ -1084,7 +1084,7 @@ struct TilePos {
 template <int C>
 __device__ __forceinline__ bool tile_pos(const StepArgs& a, TilePos& t)
 {
-    t.tile = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x / kWave);
+    t.tile = a.tile0 + (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x / kWave);
     if (t.tile >= a.ntiles) return false;
     t.base = t.tile * C * kChunk;
     const int64_t rem = (a.d - t.base + kChunk - 1) / kChunk;
@@ -1190,6 +1190,91 @@ __device__ __forceinline__ void worker_round(const StepArgs& a, const TilePos (&
     worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, i, r, slots, G, w);
 }
 
+// 8-chunk tiles whose server bucket is the whole tile (a scaled or sign
+// quantizer fixed at compile time): the server side runs on 8 waves, one
+// chunk each, instead of one wave holding all eight chunks' rows (ResNet-18-
+// sized round 0.315 -> 0.305 ms; BERT-sized, sign 2048, 16 workers 10.8 -> 5.0
+// ms).  For 4-chunk tiles it measured slower (GPT-2-medium-sized 8.13 ->
+// 8.36 ms): the waves that do not serve wait at its two barriers.
+template <class QT, int C>
+struct SplitServe {
+    static constexpr bool value = false;
+};
+template <int K, int B, int NM, int CPB, int C>
+struct SplitServe<QCt<K, B, NM, CPB>, C> {
+    static constexpr bool value = C == 8 && CPB == C && (K == Q_SCALED_SIGN || K == Q_STOCH || K == Q_DET);
+};
+// The same quantizer with its scale given (computed by the waves together).
+template <class QT>
+struct GivenScale;
+template <int K, int B, int NM, int CPB>
+struct GivenScale<QCt<K, B, NM, CPB>> {
+    using type = QCt<K, B, NM, 0>;
+};
+
+// Add chunk ch of the cnt handoff slots of a group (tiles of C chunks), in
+// ascending worker order.
+template <int C>
+__device__ __forceinline__ void gather_chunk(const float4* slot, int cnt, int ch, float4& acc)
+{
+    const int lane = lane_id();
+    for (int j = 0; j < cnt; ++j) acc = add4(acc, slot[(j * C + ch) * kWave + lane]);
+}
+
+// The server side of one whole tile on C waves: wave ch gathers chunk ch of
+// the last group, runs Adam (at the server) and adds e_s on it; the lane
+// partials of the bucket norm meet in `red` ([C][64], LDS) and every serving
+// wave adds them in chunk order (the order of the one-wave round, so the
+// scale has the same bits), then quantizes its chunk under that scale and
+// applies it.  Every wave of the block takes part in both barriers.
+template <int C, bool VEC, class QS, int PL>
+__device__ __forceinline__ void serve_split(const StepArgs& a, const TilePos& t, const float* lut_s,
+                                            const float4* slots, int cnt, float4 acc, double* red)
+{
+    using QG = typename GivenScale<QS>::type;
+    const int lane = lane_id();
+    const int w = (int)(threadIdx.x / kWave);
+    const bool serving = w < C;
+    const int ch = serving ? w : 0;
+    const int64_t base = t.base + (int64_t)ch * kChunk;
+    const int norm = QS::norm(a.qs);
+    ServerRows<1> sr;
+    if (serving) load_server<1, VEC, true, PL>(a, base, 1, true, true, sr);
+    __syncthreads();                           // the last group's handoff is complete
+    float4 u[1], q[1], dq[1];
+    if (serving) {
+        gather_chunk<C>(slots, cnt, ch, acc);
+        const float4 s1[1] = {acc};
+        server_input<1, VEC, true, PL>(a, s1, base, 1, sr, u);
+        q[0] = add4(u[0], sr.e[0]);
+        Partial p;
+        p.sum = 0.0;
+        p.mx = 0.0f;
+        partial_add4(p, norm, q[0], 4);
+        red[ch * kWave + lane] = norm == S_MAX ? (double)p.mx : p.sum;
+    }
+    __syncthreads();                           // every chunk's partial is in LDS
+    if (!serving) return;
+    double tot = 0.0;
+    float mx = 0.0f;
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+        if (norm == S_MAX) mx = fmaxf(mx, (float)red[j * kWave + lane]);
+        else tot += red[j * kWave + lane];
+    }
+    const double S = norm == S_MAX ? 0.0 : wave_sum(tot);
+    const float M = norm == S_MAX ? wave_max(mx) : 0.0f;
+    const float scale = scale_from(norm, S, M, a.qs.B);
+    if (ch == 0 && lane == 0) a.sscales[(t.base >> 8) >> QS::cpb_shift(a.qs)] = scale;
+    WordSink sink = message_sink<QG>(a.qs, a.scodes, base);
+    quantize_tile<1, true, QG>(a.qs, lut_s, q, base, 1, a.d, a.k0, a.k1, a.t, kServerStream, scale, a.scodes,
+                               a.sscales, sink, dq);
+    sink.flush();
+    const int64_t n = base + 4 * lane;
+    st4<VEC, true>(a.e_s, n, a.d, a.qs.ef ? sub4(q[0], dq[0]) : zero4());
+    st4<VEC, true>(a.x, n, a.d, sub4(sr.x[0], dq[0]));
+}
+
 // ---------------------------------------------------------------------------
 // The fused round on nt <= K consecutive tiles per block.  The block has
 // G = min(N, 16) waves.  Workers are taken in groups of G: wave w compresses
@@ -1209,19 +1294,30 @@ __device__ __forceinline__ void worker_round(const StepArgs& a, const TilePos (&
 // ---------------------------------------------------------------------------
 template <int C, int K, bool VEC, bool FULL, class QW, class QS, int PL, bool PIPE>
 __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, int nt, const float* lut_w,
-                                            const float* lut_s, float4* xfer, int G)
+                                            const float* lut_s, float4* xfer, int G, double* red)
 {
     const int lane = lane_id();
     const int w = (int)(threadIdx.x / kWave);
     const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
+    // The server side on C waves, one chunk each (the launch gives the block
+    // at least C waves); otherwise wave k serves tile k.
+    constexpr bool kSplit = SplitServe<QS, C>::value && FULL && K == 1;
 
     TilePos tp[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) tp[k] = tile_at<C>(a, tile0 + k);
 
-    float4 acc[C];
+    constexpr int kAcc = kSplit ? 1 : C;
+    float4 acc[kAcc];
 #pragma unroll
-    for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
+    for (int ch = 0; ch < kAcc; ++ch) acc[ch] = zero4();
+    const auto gather = [&](const float4* grp, int cnt) {
+        if constexpr (kSplit) {
+            if (w < C) gather_chunk<C>(grp, cnt, w, acc[0]);
+        } else {
+            if (w < nt) gather_group<C>(grp + (int64_t)w * G * C * kWave, cnt, acc);
+        }
+    };
 
     // Handoff layout: [group buffer][tile][wave][chunk][lane].  With more
     // workers than waves, PIPE kernels load a wave's next worker's rows as
@@ -1239,7 +1335,7 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
             worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, rows, slots, G, w);
             if (g0 + G + w < a.N) worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, g0 + G + w, rows);
             __syncthreads();
-            if (w < nt) gather_group<C>(slots + (int64_t)w * G * C * kWave, G, acc);
+            gather(slots, G);
         }
         slots = xfer + buf * per_buf;
         if (g0 + w < a.N) {
@@ -1251,11 +1347,15 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
             slots = xfer + buf * per_buf;
             worker_round<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
             __syncthreads();
-            if (w < nt) gather_group<C>(slots + (int64_t)w * G * C * kWave, G, acc);
+            gather(slots, G);
         }
         slots = xfer + buf * per_buf;
         if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
     }
+    if constexpr (kSplit) {
+        serve_split<C, VEC, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0], red);
+        return;
+    } else {
     const TilePos t = tile_at<C>(a, tile0 + (w < nt ? w : 0));
     ServerRows<C> sr;
     if (w < nt) load_server<C, VEC, FULL, PL>(a, t.base, t.nch, true, !sglobal, sr);
@@ -1285,6 +1385,7 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
         const int64_t n = t.base + (int64_t)ch * kChunk + 4 * lane;
         st4<VEC, FULL>(a.e_s, n, a.d, a.qs.ef ? sub4(q[ch], dq[ch]) : zero4());
         st4<VEC, FULL>(a.x, n, a.d, sub4(sr.x[ch], dq[ch]));
+    }
     }
 }
 
@@ -1325,16 +1426,19 @@ __global__ __launch_bounds__(kBlock) void worker_kernel(StepArgs a)
 }
 
 // Split call: dequantize the N worker messages, average in ascending worker
-// order, run Adam at the server if placed there; result in a.ubuf.
-template <int C, bool VEC, class QW = QRt>
+// order, run Adam at the server if placed there; result in a.ubuf.  FULL:
+// every tile of the launch lies wholly inside d (no per-tile checks).
+template <int C, bool VEC, class QW = QRt, bool FULL = false>
 __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
 {
+    static_assert(!FULL || VEC, "whole-tile kernels need aligned rows");
     __shared__ float lut_w[kLutSize];
     __shared__ __attribute__((aligned(16))) uint32_t stage_all[kWavesPerBlock][stage_words<C, QW>()];
     fill_lut(a.qw, lut_w);
     __syncthreads();
     TilePos t;
     if (!tile_pos<C>(a, t)) return;
+    const int nch = FULL ? C : t.nch;
     uint32_t* stage = stage_all[threadIdx.x / kWave];
     const int lane = lane_id();
     float4 acc[C], dq[C], u[C];
@@ -1346,23 +1450,23 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
     CodeWords<C, QW> wv;
     float sc[C];
     if (planes) {
-        load_code_words<C, QW>(a.qw, a.wcodes, t.base, t.nch, wv);
-        load_chunk_scales<C, QW>(a.qw, a.wscales, t.base, t.nch, sc);
+        load_code_words<C, QW>(a.qw, a.wcodes, t.base, nch, wv);
+        load_chunk_scales<C, QW>(a.qw, a.wscales, t.base, nch, sc);
     }
     for (int i = 0; i < a.N; ++i) {
         if (planes) {
             const int64_t j = i + 1 < a.N ? i + 1 : i;
             CodeWords<C, QW> nwv;
             float nsc[C];
-            load_code_words<C, QW>(a.qw, a.wcodes + j * a.qw.words, t.base, t.nch, nwv);
-            load_chunk_scales<C, QW>(a.qw, a.wscales + j * a.qw.nscales, t.base, t.nch, nsc);
-            decode_words<C, QW, true>(a.qw, lut_w, wv, sc, t.base, t.nch, a.d, stage, dq);
+            load_code_words<C, QW>(a.qw, a.wcodes + j * a.qw.words, t.base, nch, nwv);
+            load_chunk_scales<C, QW>(a.qw, a.wscales + j * a.qw.nscales, t.base, nch, nsc);
+            decode_words<C, QW, true>(a.qw, lut_w, wv, sc, t.base, nch, a.d, stage, dq);
             wv = nwv;
 #pragma unroll
             for (int ch = 0; ch < C; ++ch) sc[ch] = nsc[ch];
         } else {
             dequant_tile<C, QW>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
-                                 a.wscales + (int64_t)i * a.qw.nscales, t.base, t.nch, a.d, stage, dq);
+                                 a.wscales + (int64_t)i * a.qw.nscales, t.base, nch, a.d, stage, dq);
         }
 #pragma unroll
         for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
@@ -1370,11 +1474,11 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
     // The server's rows load after the decoding: held through it, they cost
     // occupancy (BERT-sized 4-bit, 16 workers: 843 -> 817 us).
     ServerRows<C> sr;
-    load_server<C, VEC, false, -1>(a, t.base, t.nch, false, false, sr);
-    server_input<C, VEC, false, -1>(a, acc, t.base, t.nch, sr, u);
+    load_server<C, VEC, FULL, -1>(a, t.base, nch, false, false, sr);
+    server_input<C, VEC, FULL, -1>(a, acc, t.base, nch, sr, u);
 #pragma unroll
     for (int ch = 0; ch < C; ++ch)
-        if (ch < t.nch) st4<VEC>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
+        if (FULL || ch < nch) st4<VEC, FULL>(a.ubuf, t.base + (int64_t)ch * kChunk + 4 * lane, a.d, u[ch]);
 }
 
 
@@ -1512,9 +1616,10 @@ __global__ __launch_bounds__(max_round_waves(C) * kWave,
     }
     float4* xfer = smem + table_floats(G) / 4;
     constexpr int K = kernel_tiles(C, FULL, PL, half_kernel<QW, QS, PL>());
+    __shared__ double red[SplitServe<QS, C>::value && FULL && K == 1 ? C * kWave : 1];
     const int64_t first = a.tile0 + (int64_t)blockIdx.x * K;
     const int64_t left = a.tile1 - first;
-    round_tiles<C, K, VEC, FULL, QW, QS, PL, PIPE>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G);
+    round_tiles<C, K, VEC, FULL, QW, QS, PL, PIPE>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G, red);
 }
 
 }  // namespace

@@ -187,6 +187,37 @@ def test_one_chunk_tiles_worker_groups(N):
     _run(d, N, SIGN(256), qfields(O.Q_TOPK, bucket=256, keep=9), O.ADAM_AT_SERVER, T=2)
 
 
+WIDE = {
+    "sign": lambda b: SIGN(b),
+    "stoch4_l2": lambda b: STOCH(4, O.SCALE_L2, b),
+    "stoch2_max": lambda b: STOCH(2, O.SCALE_MAX, b),
+    "stoch1_l2": lambda b: STOCH(1, O.SCALE_L2, b),
+    "stoch8_max": lambda b: STOCH(8, O.SCALE_MAX, b),
+}
+
+
+@pytest.mark.parametrize("bucket", [1024, 2048])
+@pytest.mark.parametrize("kind", list(WIDE))
+def test_wide_tiles_same_quantizer(kind, bucket):
+    """Buckets of 4 and 8 chunks with the same quantizer on both sides and
+    Adam at the server: fully specialized kernels whose server side runs on
+    one wave per chunk, with fewer workers than chunks (the block then has
+    more waves than workers), as many, and more (two worker groups)."""
+    q = WIDE[kind](bucket)
+    for N in (3, bucket // 256, bucket // 256 + 5):
+        _run(bucket * 5 + 700, N, q, q, O.ADAM_AT_SERVER, T=3)
+
+
+@pytest.mark.parametrize("N", [1, 2, 8, 13])
+def test_wide_specialized_workload_kernels(N):
+    """The ResNet-18- and GPT-2-medium-sized rounds' kernels (sign 2048 both
+    sides; stochastic 2-bit max-norm 1024 / sign 1024) with worker counts
+    around the block's waves, both placements."""
+    for pl in (O.ADAM_AT_SERVER, O.ADAM_AT_WORKER):
+        _run(2048 * 6 + 1576, N, SIGN(2048), SIGN(2048), pl, T=3, gen="segscale")
+        _run(1024 * 7 + 704, N, STOCH(2, O.SCALE_MAX, 1024), SIGN(1024), pl, T=3, gen="outliers")
+
+
 EXTREME_KINDS = {
     "stoch4_l2": STOCH(4, O.SCALE_L2, 512),
     "stoch2_max": STOCH(2, O.SCALE_MAX, 512),
