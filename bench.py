@@ -70,12 +70,13 @@ def split_bytes(E, cfg) -> int:
     return algorithmic_bytes(E, cfg) + N * (8 * ww + 4 * nw) + 8 * d + 8 * sw + 4 * ns
 
 
-def traffic_from_profile(workload: str, placement: str):
+def traffic_from_profile(workload: str, placement: str, call: str = "step"):
     """HBM bytes per round measured by rocprofv3 counters (FETCH_SIZE and
-    WRITE_SIZE summed over the round's step_kernel launches, each scaled by
-    what it reads for a plain copy of known size), if the committed counter
-    summary was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", f"step_kernel_{workload}_{placement}_pmc.txt")
+    WRITE_SIZE summed over the round's launches of the library's kernels,
+    each scaled by what it reads for a plain copy of known size), if the
+    committed counter summary was taken on the current kernel sources."""
+    kind = "split_calls" if call == "split" else "step_kernel"
+    path = os.path.join(ROOT, "profiles", f"{kind}_{workload}_{placement}_pmc.txt")
     if not os.path.exists(path):
         return None
     rec = {}
@@ -326,7 +327,8 @@ def main():
     value = cfg.d / (ms * 1e-3) / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4),
-            "traffic": None if args.call == "split" else traffic_from_profile(args.workload, args.placement),
+            "traffic": (traffic_from_profile(args.workload, args.placement, args.call)
+                        if args.call in ("step", "split") else None),
             "kernel": ("worker_kernel x N, aggregate_kernel, server_kernel, apply_kernel" if args.call == "split"
                        else "step_kernel (whole tiles + ragged tail)"),
             "algorithmic_bytes_per_round": alg,
