@@ -1180,14 +1180,31 @@ __device__ __forceinline__ void worker_tiles(const StepArgs& a, const TilePos (&
     sink.flush();
 }
 
-// Worker i on the block's tiles: its rows are loaded, then compressed.
-template <int C, int K, bool VEC, bool FULL, class QW, int PL>
+// Worker i on the block's tiles: its rows are loaded, then compressed.  The
+// two spellings take the same steps; the register allocator does better with
+// the first on fully specialized whole-tile kernels (BERT-sized round 94 -> 89
+// VGPRs, random-k 96 with a 24-byte spill -> 95 without) and with the second
+// on the others (the generic 8-chunk kernel spills with the first).
+template <int C, int K, bool VEC, bool FULL, class QW, int PL, bool INLINE>
 __device__ __forceinline__ void worker_round(const StepArgs& a, const TilePos (&tp)[K], int nt, const float* lut_w,
                                              int i, float4* slots, int G, int w)
 {
     WorkerRows<C> r[K];
-    worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, i, r);
-    worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, i, r, slots, G, w);
+    if constexpr (INLINE) {
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+            if (k < nt) worker_load<C, VEC, FULL, PL>(a, tp[k], i, r[k]);
+        WordSink sink = message_sink<QW>(a.qw, a.wcodes + (int64_t)i * a.qw.words, tp[0].base);
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+            if (k < nt)
+                worker_compute<C, VEC, FULL, QW, PL>(a, tp[k], lut_w, i, r[k], sink,
+                                                     slots + ((int64_t)k * G + w) * C * kWave);
+        sink.flush();
+    } else {
+        worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, i, r);
+        worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, i, r, slots, G, w);
+    }
 }
 
 // 8-chunk tiles whose server bucket is the whole tile (a scaled or sign
@@ -1343,14 +1360,15 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
             worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, rows, slots, G, w);
         }
     } else {
+        constexpr bool kInline = FULL && QW::fixed && QS::fixed;
         for (; g0 + G < a.N; g0 += G, buf ^= 1) {
             slots = xfer + buf * per_buf;
-            worker_round<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
+            worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
             __syncthreads();
             gather(slots, G);
         }
         slots = xfer + buf * per_buf;
-        if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, slots, G, w);
+        if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
     }
     if constexpr (kSplit) {
         serve_split<C, VEC, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0], red);
