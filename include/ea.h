@@ -12,7 +12,12 @@
  *     are host memory read during the call only.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream)
  *     and the call returns without waiting.  Errors raised by the device
- *     surface at the next synchronization of that stream.
+ *     surface at the next synchronization of that stream.  The fused round
+ *     (ea_step, ea_step_scheduled, ea_run) may run the ragged last tile on a
+ *     stream of its own (default priority, one per device, created on first
+ *     use), forked from `stream` and joined back to it within the call, so
+ *     work queued on `stream` afterwards still sees every result; not while
+ *     `stream` is being captured, and never in ea_step_noalloc.
  *   - Return value: EA_OK, or a negative EA_ERR_* code; ea_last_error()
  *     returns a description of the last failure on the calling thread.
  *     Arguments are validated before any device work is enqueued, so an

@@ -317,7 +317,8 @@ bool vec_ok(int64_t d, std::initializer_list<const void*> ptrs)
 // come from the schedule at that step, and t_dev is advanced afterwards.
 int step_impl(const char* name, const ea_config_t* c, int64_t t, uint32_t* t_dev, const ea_schedule_t* sched,
               const float* g, float* e_w, float* m_w, float* v_w, float* m, float* v, float* e_s, float* x,
-              uint64_t* wcodes, float* wscales, uint64_t* scodes, float* sscales, void* workspace, void* stream)
+              uint64_t* wcodes, float* wscales, uint64_t* scodes, float* sscales, void* workspace, void* stream,
+              bool side_stream = true)
 {
     Plan p;
     int rc = make_plan(c, &p);
@@ -378,7 +379,7 @@ int step_impl(const char* name, const ea_config_t* c, int64_t t, uint32_t* t_dev
         if (e == hipSuccess)
             e = ea::launch_finalize(a.wpart, p.ntiles, p.qw.norm, c->d, wscales, p.qw.nscales, c->N, s);
     }
-    if (e == hipSuccess) e = ea::launch_step(a, p.C, vec, s);
+    if (e == hipSuccess) e = ea::launch_step(a, p.C, vec, s, side_stream);
     if (e == hipSuccess && p.sglobal) {
         e = ea::launch_finalize(a.spart, p.ntiles, p.qs.norm, c->d, sscales, 1, 1, s);
         if (e == hipSuccess) e = ea::launch_server(a, p.C, vec, s);
@@ -619,8 +620,9 @@ int ea_step_noalloc(const ea_config_t* c, int64_t t, const float* g, float* e_w,
                     (long long)p.ws_bytes, (long long)kScratchBytes);
     void* ws = nullptr;
     if (p.ws_bytes > 0 && (rc = scratch_ptr(&ws))) return rc;
+    // no side stream for the ragged tile: creating one on first use would allocate
     return step_impl("ea_step_noalloc", c, t, nullptr, nullptr, g, e_w, m_w, v_w, m, v, e_s, x, wcodes, wscales,
-                     scodes, sscales, ws, stream);
+                     scodes, sscales, ws, stream, false);
 }
 
 int ea_schedule_at(const ea_config_t* c, const ea_schedule_t* s, int64_t t, float* lr, float* beta2)

@@ -3,6 +3,8 @@
 // matches a configuration).  The round itself is in ea_round.hpp.
 #include "ea_round.hpp"
 
+#include <mutex>
+
 namespace ea {
 
 namespace {
@@ -207,75 +209,166 @@ const SymKernel* find_sym(const StepArgs& a, int C)
 
 }  // namespace
 
+namespace {
+
+hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
+                            const HalfKernel* hk, size_t limit, hipStream_t s);
+hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
+                            size_t limit, hipStream_t s);
+
+// Tiles per block of the whole-tile launch.
+int main_tiles_per_block(int C, const Special* sp, const SymKernel* sk, const HalfKernel* hk)
+{
+    return sp ? sp->tiles : sk ? sk->tiles : hk ? hk->tiles : round_tiles_per_block(C, false);
+}
+
+// A second stream per device for the ragged last tile (see launch_step).
+// Default priority, non-blocking with respect to the null stream.
+struct SideStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    bool tried = false, ok = false;
+};
+constexpr int kMaxSideDevices = 64;
+std::mutex g_side_mu;
+SideStream g_side[kMaxSideDevices];
+
+// The current device's side stream, created on first use; nullptr if it
+// cannot be had.  Called with g_side_mu held.
+SideStream* device_side_stream()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxSideDevices) return nullptr;
+    SideStream& ss = g_side[dev];
+    if (!ss.tried) {
+        ss.tried = true;
+        ss.ok = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking) == hipSuccess &&
+                hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) == hipSuccess &&
+                hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) == hipSuccess;
+    }
+    return ss.ok ? &ss : nullptr;
+}
+
+}  // namespace
+
 // Whole tiles go to a kernel without bounds checks: one specialized for both
 // quantizers and the placement when one matches, else one specialized for
 // the worker quantizer, else the generic one.  The ragged last tile goes to a
 // checked kernel, specialized in the first case.  Every tile of rows that are
 // not 16-byte aligned goes to the generic checked kernel.
-hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s)
+//
+// The ragged tile is one block whose latency would add in full to the round
+// if it were queued behind the whole-tile launch (about 23 us of a 0.31 ms
+// ResNet-18-sized round).  The two launches touch disjoint elements, message
+// words and scales, so the ragged tile runs on a side stream forked from the
+// caller's stream before both launches and joined back after them; the
+// caller's stream then holds both.  That pays while the whole-tile launch is
+// short (ResNet-18-sized round 0.306 -> 0.296 ms, ResNet-50-sized 2.160 ->
+// 2.130 ms); on the long launches it did not (BERT-sized unchanged at 4.57
+// ms, GPT-2-medium-sized 7.83 -> 7.93 ms), so those queue both launches in
+// order, as does every launch under stream capture.
+constexpr int64_t kSideStreamMaxBlocks = 32768;
+
+hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s, bool side_stream)
 {
     const size_t limit = lds_limit_bytes();
     const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) : 0;
     const Special* sp = vec ? find_special(a, C) : nullptr;
     const SymKernel* sk = vec && !sp ? find_sym(a, C) : nullptr;
     const HalfKernel* hk = vec && !sp && !sk ? find_half(a, C) : nullptr;
-    if (nfull > 0) {
-        const int K = sp ? sp->tiles : sk ? sk->tiles : hk ? hk->tiles : round_tiles_per_block(C, false);
-        int G = round_waves(a.N, C, K, limit, a.placement);
-        // fully specialized wide tiles serve the whole-tile server bucket on C
-        // waves, one chunk each (SplitServe), so their blocks have C waves at least
-        const bool split = (sp || sk) && C == 8 && a.qs.cpb == C &&
-                           (a.qs.kind == Q_SCALED_SIGN || a.qs.kind == Q_STOCH || a.qs.kind == Q_DET);
-        if (split && G < C) G = C;
-        StepArgs b = a;
-        b.tile0 = 0;
-        b.tile1 = nfull;
-        const dim3 grid((unsigned)((nfull + K - 1) / K)), block((unsigned)(G * kWave));
-        const size_t lds = round_lds_bytes(a.N, C, G, K);
-        if (sp) {
-            hipLaunchKernelGGL(a.N > G ? sp->many : sp->kernel, grid, block, lds, s, b);
-        } else if (sk) {
-            hipLaunchKernelGGL(sk->kernel, grid, block, lds, s, b);
-        } else if (hk) {
-            hipLaunchKernelGGL(hk->kernel, grid, block, lds, s, b);
-        } else {
-            switch (C) {
-            case 1: hipLaunchKernelGGL((step_kernel<1, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-            case 2: hipLaunchKernelGGL((step_kernel<2, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-            case 4: hipLaunchKernelGGL((step_kernel<4, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-            case 8: hipLaunchKernelGGL((step_kernel<8, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-            default: return hipErrorInvalidValue;
+    const bool has_main = nfull > 0, has_edge = nfull < a.ntiles;
+    const int K = main_tiles_per_block(C, sp, sk, hk);
+    const int64_t main_blocks = (nfull + K - 1) / K;
+    if (side_stream && has_main && has_edge && main_blocks < kSideStreamMaxBlocks) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusActive;
+        if (hipStreamIsCapturing(s, &cs) == hipSuccess && cs == hipStreamCaptureStatusNone) {
+            std::lock_guard<std::mutex> lock(g_side_mu);
+            if (SideStream* ss = device_side_stream()) {
+                hipError_t e = hipEventRecord(ss->fork, s);
+                if (e == hipSuccess) e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
+                if (e != hipSuccess) return e;
+                e = launch_step_edge(a, C, nfull, sp, sk, limit, ss->stream);
+                if (e == hipSuccess) e = launch_step_main(a, C, nfull, sp, sk, hk, limit, s);
+                // joined even after a failed launch, so that s never runs ahead of the side stream
+                const hipError_t r = hipEventRecord(ss->join, ss->stream);
+                const hipError_t w = r == hipSuccess ? hipStreamWaitEvent(s, ss->join, 0) : r;
+                return e != hipSuccess ? e : w;
             }
         }
-        const hipError_t e = hipGetLastError();
+    }
+    if (has_main) {
+        const hipError_t e = launch_step_main(a, C, nfull, sp, sk, hk, limit, s);
         if (e != hipSuccess) return e;
     }
-    if (nfull < a.ntiles) {
-        const int G = round_waves(a.N, C, 1, limit, a.placement);
-        StepArgs b = a;
-        b.tile0 = nfull;
-        b.tile1 = a.ntiles;
-        const dim3 grid((unsigned)(a.ntiles - nfull)), block((unsigned)(G * kWave));
-        const size_t lds = round_lds_bytes(a.N, C, G, 1);
-        if (sp) {
-            hipLaunchKernelGGL(sp->edge, grid, block, lds, s, b);
-            return hipGetLastError();
-        }
-        if (sk) {
-            hipLaunchKernelGGL(sk->edge, grid, block, lds, s, b);
-            return hipGetLastError();
-        }
+    return has_edge ? launch_step_edge(a, C, nfull, sp, sk, limit, s) : hipSuccess;
+}
+
+namespace {
+
+// The whole tiles [0, nfull) of a round (launch_step).
+hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
+                            const HalfKernel* hk, size_t limit, hipStream_t s)
+{
+    const int K = main_tiles_per_block(C, sp, sk, hk);
+    int G = round_waves(a.N, C, K, limit, a.placement);
+    // fully specialized wide tiles serve the whole-tile server bucket on C
+    // waves, one chunk each (SplitServe), so their blocks have C waves at least
+    const bool split = (sp || sk) && C == 8 && a.qs.cpb == C &&
+                       (a.qs.kind == Q_SCALED_SIGN || a.qs.kind == Q_STOCH || a.qs.kind == Q_DET);
+    if (split && G < C) G = C;
+    StepArgs b = a;
+    b.tile0 = 0;
+    b.tile1 = nfull;
+    const dim3 grid((unsigned)((nfull + K - 1) / K)), block((unsigned)(G * kWave));
+    const size_t lds = round_lds_bytes(a.N, C, G, K);
+    if (sp) {
+        hipLaunchKernelGGL(a.N > G ? sp->many : sp->kernel, grid, block, lds, s, b);
+    } else if (sk) {
+        hipLaunchKernelGGL(sk->kernel, grid, block, lds, s, b);
+    } else if (hk) {
+        hipLaunchKernelGGL(hk->kernel, grid, block, lds, s, b);
+    } else {
         switch (C) {
-        case 1: hipLaunchKernelGGL((step_kernel<1, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
-        case 2: hipLaunchKernelGGL((step_kernel<2, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
-        case 4: hipLaunchKernelGGL((step_kernel<4, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
-        case 8: hipLaunchKernelGGL((step_kernel<8, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        case 1: hipLaunchKernelGGL((step_kernel<1, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        case 2: hipLaunchKernelGGL((step_kernel<2, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        case 4: hipLaunchKernelGGL((step_kernel<4, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+        case 8: hipLaunchKernelGGL((step_kernel<8, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
         default: return hipErrorInvalidValue;
         }
+    }
+    return hipGetLastError();
+}
+
+// The tiles [nfull, ntiles) of a round, one block each, with bounds checks
+// (launch_step).
+hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
+                            size_t limit, hipStream_t s)
+{
+    const int G = round_waves(a.N, C, 1, limit, a.placement);
+    StepArgs b = a;
+    b.tile0 = nfull;
+    b.tile1 = a.ntiles;
+    const dim3 grid((unsigned)(a.ntiles - nfull)), block((unsigned)(G * kWave));
+    const size_t lds = round_lds_bytes(a.N, C, G, 1);
+    if (sp) {
+        hipLaunchKernelGGL(sp->edge, grid, block, lds, s, b);
         return hipGetLastError();
     }
-    return hipSuccess;
+    if (sk) {
+        hipLaunchKernelGGL(sk->edge, grid, block, lds, s, b);
+        return hipGetLastError();
+    }
+    switch (C) {
+    case 1: hipLaunchKernelGGL((step_kernel<1, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+    case 2: hipLaunchKernelGGL((step_kernel<2, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+    case 4: hipLaunchKernelGGL((step_kernel<4, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+    case 8: hipLaunchKernelGGL((step_kernel<8, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
+
+}  // namespace
 
 hipError_t launch_worker_partials(const StepArgs& a, int C, bool vec, int i0, int i1, hipStream_t s)
 {

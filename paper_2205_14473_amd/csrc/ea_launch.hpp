@@ -51,7 +51,9 @@ struct StepArgs {
 };
 
 // Launchers; C = chunks per tile (1..8), vec = rows are 16-byte aligned.
-hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s);
+// side_stream: the ragged last tile may run on a library-owned stream forked
+// from s and joined back to it (created on first use per device).
+hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s, bool side_stream = true);
 
 // Kernels specialized for the worker quantizer only (kind, code bits, norm
 // and chunks per bucket fixed; the server quantizer and the Adam placement
