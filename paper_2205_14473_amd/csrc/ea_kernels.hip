@@ -272,13 +272,16 @@ constexpr int64_t kSideStreamMaxBlocks = 32768;
 hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s, bool side_stream)
 {
     const size_t limit = lds_limit_bytes();
-    const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) : 0;
     const Special* sp = vec ? find_special(a, C) : nullptr;
     const SymKernel* sk = vec && !sp ? find_sym(a, C) : nullptr;
     const HalfKernel* hk = vec && !sp && !sk ? find_half(a, C) : nullptr;
-    const bool has_main = nfull > 0, has_edge = nfull < a.ntiles;
+    // The whole-tile launch takes a multiple of its tiles per block (its
+    // kernels assume full blocks); the whole tiles left over go to the checked
+    // launch with the ragged one.
     const int K = main_tiles_per_block(C, sp, sk, hk);
-    const int64_t main_blocks = (nfull + K - 1) / K;
+    const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) / K * K : 0;
+    const bool has_main = nfull > 0, has_edge = nfull < a.ntiles;
+    const int64_t main_blocks = nfull / K;
     if (side_stream && has_main && has_edge && main_blocks < kSideStreamMaxBlocks) {
         hipStreamCaptureStatus cs = hipStreamCaptureStatusActive;
         if (hipStreamIsCapturing(s, &cs) == hipSuccess && cs == hipStreamCaptureStatusNone) {
@@ -305,7 +308,8 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s, bool s
 
 namespace {
 
-// The whole tiles [0, nfull) of a round (launch_step).
+// The whole tiles [0, nfull) of a round, nfull a multiple of the kernel's
+// tiles per block (launch_step).
 hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
                             const HalfKernel* hk, size_t limit, hipStream_t s)
 {
@@ -319,7 +323,7 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
     StepArgs b = a;
     b.tile0 = 0;
     b.tile1 = nfull;
-    const dim3 grid((unsigned)((nfull + K - 1) / K)), block((unsigned)(G * kWave));
+    const dim3 grid((unsigned)(nfull / K)), block((unsigned)(G * kWave));
     const size_t lds = round_lds_bytes(a.N, C, G, K);
     if (sp) {
         hipLaunchKernelGGL(a.N > G ? sp->many : sp->kernel, grid, block, lds, s, b);
@@ -339,7 +343,8 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
     return hipGetLastError();
 }
 
-// The tiles [nfull, ntiles) of a round, one block each, with bounds checks
+// The tiles [nfull, ntiles) of a round (at most one short of a whole-tile
+// block, plus the ragged one), one block each, with bounds checks
 // (launch_step).
 hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
                             size_t limit, hipStream_t s)

@@ -1319,6 +1319,13 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
     // The server side on C waves, one chunk each (the launch gives the block
     // at least C waves); otherwise wave k serves tile k.
     constexpr bool kSplit = SplitServe<QS, C>::value && FULL && K == 1;
+    // Whole-tile launches give every block exactly K tiles.  With that known
+    // at compile time, each wave's loads of all K tiles and its work on them
+    // are straight-line code, so the compiler waits for each tile's rows
+    // only before that tile's arithmetic.  (With the later tiles under a
+    // branch it waited for every load, and for the stores issued since,
+    // before the first tile and again before the second.)
+    if constexpr (FULL && !PIPE) nt = K;
 
     TilePos tp[K];
 #pragma unroll
