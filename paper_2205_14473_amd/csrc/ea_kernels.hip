@@ -249,6 +249,34 @@ SideStream* device_side_stream()
     return ss.ok ? &ss : nullptr;
 }
 
+// Runs main(s) and edge(t): with `allow` and when s is not being captured, t
+// is the device's side stream, forked from s before both launches and joined
+// back to s after them; otherwise both go to s in order.  main and edge must
+// touch disjoint memory.
+template <class Main, class Edge>
+hipError_t run_beside(hipStream_t s, bool allow, const Main& main, const Edge& edge)
+{
+    if (allow) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusActive;
+        if (hipStreamIsCapturing(s, &cs) == hipSuccess && cs == hipStreamCaptureStatusNone) {
+            std::lock_guard<std::mutex> lock(g_side_mu);
+            if (SideStream* ss = device_side_stream()) {
+                hipError_t e = hipEventRecord(ss->fork, s);
+                if (e == hipSuccess) e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
+                if (e != hipSuccess) return e;
+                e = edge(ss->stream);
+                if (e == hipSuccess) e = main(s);
+                // joined even after a failed launch, so that s never runs ahead of the side stream
+                const hipError_t r = hipEventRecord(ss->join, ss->stream);
+                const hipError_t w = r == hipSuccess ? hipStreamWaitEvent(s, ss->join, 0) : r;
+                return e != hipSuccess ? e : w;
+            }
+        }
+    }
+    const hipError_t e = main(s);
+    return e == hipSuccess ? edge(s) : e;
+}
+
 }  // namespace
 
 // Whole tiles go to a kernel without bounds checks: one specialized for both
@@ -282,27 +310,12 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s, bool s
     const int64_t nfull = vec ? a.d / ((int64_t)C * kChunk) / K * K : 0;
     const bool has_main = nfull > 0, has_edge = nfull < a.ntiles;
     const int64_t main_blocks = nfull / K;
-    if (side_stream && has_main && has_edge && main_blocks < kSideStreamMaxBlocks) {
-        hipStreamCaptureStatus cs = hipStreamCaptureStatusActive;
-        if (hipStreamIsCapturing(s, &cs) == hipSuccess && cs == hipStreamCaptureStatusNone) {
-            std::lock_guard<std::mutex> lock(g_side_mu);
-            if (SideStream* ss = device_side_stream()) {
-                hipError_t e = hipEventRecord(ss->fork, s);
-                if (e == hipSuccess) e = hipStreamWaitEvent(ss->stream, ss->fork, 0);
-                if (e != hipSuccess) return e;
-                e = launch_step_edge(a, C, nfull, sp, sk, limit, ss->stream);
-                if (e == hipSuccess) e = launch_step_main(a, C, nfull, sp, sk, hk, limit, s);
-                // joined even after a failed launch, so that s never runs ahead of the side stream
-                const hipError_t r = hipEventRecord(ss->join, ss->stream);
-                const hipError_t w = r == hipSuccess ? hipStreamWaitEvent(s, ss->join, 0) : r;
-                return e != hipSuccess ? e : w;
-            }
-        }
-    }
-    if (has_main) {
-        const hipError_t e = launch_step_main(a, C, nfull, sp, sk, hk, limit, s);
-        if (e != hipSuccess) return e;
-    }
+    if (has_main && has_edge)
+        return run_beside(
+            s, side_stream && main_blocks < kSideStreamMaxBlocks,
+            [&](hipStream_t t) { return launch_step_main(a, C, nfull, sp, sk, hk, limit, t); },
+            [&](hipStream_t t) { return launch_step_edge(a, C, nfull, sp, sk, limit, t); });
+    if (has_main) return launch_step_main(a, C, nfull, sp, sk, hk, limit, s);
     return has_edge ? launch_step_edge(a, C, nfull, sp, sk, limit, s) : hipSuccess;
 }
 
@@ -418,19 +431,28 @@ hipError_t launch_aggregate(const StepArgs& a, int C, bool vec, hipStream_t s)
     const HalfKernel* hk = vec ? find_half(a, C) : nullptr;
     if (hk) {
         const int64_t nfull = C <= 4 ? a.d / ((int64_t)C * kChunk) : 0;
-        if (nfull > 0) {
+        const auto full = [&](hipStream_t t) {
             StepArgs b = a;
             b.tile0 = 0;
             b.ntiles = nfull;
-            hipLaunchKernelGGL(hk->aggregate_full, dim3((unsigned)grid_of(b)), dim3(kBlock), 0, s, b);
-            const hipError_t e = hipGetLastError();
+            hipLaunchKernelGGL(hk->aggregate_full, dim3((unsigned)grid_of(b)), dim3(kBlock), 0, t, b);
+            return hipGetLastError();
+        };
+        const auto rest = [&](hipStream_t t) {
+            StepArgs b = a;
+            b.tile0 = nfull;
+            hipLaunchKernelGGL(hk->aggregate, dim3((unsigned)((a.ntiles - nfull + kWavesPerBlock - 1) / kWavesPerBlock)),
+                               dim3(kBlock), 0, t, b);
+            return hipGetLastError();
+        };
+        // The ragged tile stays on s after the whole tiles: on a side stream it
+        // measured slower (BERT-sized split round 4.447 -> 4.456 ms,
+        // ResNet-50-sized 2.024 -> 2.046 ms).
+        if (nfull > 0) {
+            const hipError_t e = full(s);
             if (e != hipSuccess || nfull == a.ntiles) return e;
         }
-        StepArgs b = a;
-        b.tile0 = nfull;
-        hipLaunchKernelGGL(hk->aggregate, dim3((unsigned)((a.ntiles - nfull + kWavesPerBlock - 1) / kWavesPerBlock)),
-                           dim3(kBlock), 0, s, b);
-        return hipGetLastError();
+        return rest(s);
     }
     EA_DISPATCH(aggregate_kernel, C, vec, grid_of(a), s, a);
     return hipGetLastError();
