@@ -127,21 +127,13 @@ struct Special {
     void (*kernel)(StepArgs);   // whole tiles
     void (*edge)(StepArgs);     // the ragged last tile
     int tiles;                  // tiles per block of `kernel`
-    void (*many)(StepArgs);     // whole tiles with more workers than waves
 };
-
-// Waves per SIMD of the kernels for more workers than waves: the next
-// group's rows and the sums are live together.
-#ifndef EA_PIPE_MIN_WAVES
-#define EA_PIPE_MIN_WAVES 4
-#endif
 
 #define EA_SPECIAL(CC, QWT, QST, PLC)                                                               \
     Special{CC, QWT::kind(QDev{}), QWT::bits(QDev{}), QWT::norm(QDev{}), QWT::cpb(QDev{}),         \
             QST::kind(QDev{}), QST::bits(QDev{}), QST::norm(QDev{}), QST::cpb(QDev{}), PLC,         \
             step_kernel<CC, true, true, QWT, QST, PLC>, step_kernel<CC, true, false, QWT, QST, PLC>,         \
-            round_tiles_per_block(CC, PLC == AT_SERVER),                                               \
-            step_kernel<CC, true, true, QWT, QST, PLC, EA_PIPE_MIN_WAVES, true>}
+            round_tiles_per_block(CC, PLC == AT_SERVER)}
 
 const Special kSpecials[] = {
     EA_SPECIAL(2, Stoch4L2Q2, Stoch4L2Q2, AT_SERVER),
@@ -336,10 +328,12 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
     StepArgs b = a;
     b.tile0 = 0;
     b.tile1 = nfull;
+    const int bufs = handoff_bufs(a.N, C, G, K, limit);
+    b.one_buffer = bufs == 1 ? 1 : 0;
     const dim3 grid((unsigned)(nfull / K)), block((unsigned)(G * kWave));
-    const size_t lds = round_lds_bytes(a.N, C, G, K);
+    const size_t lds = round_lds_bytes(a.N, C, G, K, bufs);
     if (sp) {
-        hipLaunchKernelGGL(a.N > G ? sp->many : sp->kernel, grid, block, lds, s, b);
+        hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
     } else if (sk) {
         hipLaunchKernelGGL(sk->kernel, grid, block, lds, s, b);
     } else if (hk) {
@@ -366,8 +360,10 @@ hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Speci
     StepArgs b = a;
     b.tile0 = nfull;
     b.tile1 = a.ntiles;
+    const int bufs = handoff_bufs(a.N, C, G, 1, limit);
+    b.one_buffer = bufs == 1 ? 1 : 0;
     const dim3 grid((unsigned)(a.ntiles - nfull)), block((unsigned)(G * kWave));
-    const size_t lds = round_lds_bytes(a.N, C, G, 1);
+    const size_t lds = round_lds_bytes(a.N, C, G, 1, bufs);
     if (sp) {
         hipLaunchKernelGGL(sp->edge, grid, block, lds, s, b);
         return hipGetLastError();

@@ -42,6 +42,7 @@ struct StepArgs {
     int64_t tile0, tile1;     // fused round: the launch's tiles [tile0, tile1)
     int32_t worker;           // split calls: worker index (Philox stream)
     int32_t apply;            // server_kernel: also update x
+    int32_t one_buffer;       // fused round, more workers than waves: single-buffered handoff
     // Step index read on the device (null: `t`, `lr`, `beta2` above hold the
     // step's values); the schedule then gives lr and beta2 at that step.
     const uint32_t* t_dev;

@@ -1309,7 +1309,7 @@ __device__ __forceinline__ void serve_split(const StepArgs& a, const TilePos& t,
 // the wait for the workers, without the loaded rows being live during the
 // earlier groups.
 // ---------------------------------------------------------------------------
-template <int C, int K, bool VEC, bool FULL, class QW, class QS, int PL, bool PIPE>
+template <int C, int K, bool VEC, bool FULL, class QW, class QS, int PL>
 __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, int nt, const float* lut_w,
                                             const float* lut_s, float4* xfer, int G, double* red)
 {
@@ -1325,7 +1325,7 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
     // only before that tile's arithmetic.  (With the later tiles under a
     // branch it waited for every load, and for the stores issued since,
     // before the first tile and again before the second.)
-    if constexpr (FULL && !PIPE) nt = K;
+    if constexpr (FULL) nt = K;
 
     TilePos tp[K];
 #pragma unroll
@@ -1344,39 +1344,23 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
     };
 
     // Handoff layout: [group buffer][tile][wave][chunk][lane].  With more
-    // workers than waves, PIPE kernels load a wave's next worker's rows as
-    // soon as it has handed its current worker over, so that they arrive
-    // during the barrier and the gather rather than after them (the rows and
-    // the sums are then live together, which costs registers).
+    // workers than waves the groups alternate between two buffers, so one
+    // barrier per group suffices; a single buffer (a.one_buffer, chosen by
+    // the launcher when two buffers would leave a CU room for only one block)
+    // takes a second barrier per group, after the gather.
     const int64_t per_buf = (int64_t)K * G * C * kWave;
     int buf = 0, g0 = 0;
     float4* slots;
-    if constexpr (PIPE) {
-        WorkerRows<C> rows[K];
-        if (w < a.N) worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, w, rows);
-        for (; g0 + G < a.N; g0 += G, buf ^= 1) {
-            slots = xfer + buf * per_buf;
-            worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, rows, slots, G, w);
-            if (g0 + G + w < a.N) worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, g0 + G + w, rows);
-            __syncthreads();
-            gather(slots, G);
-        }
+    constexpr bool kInline = FULL && QW::fixed && QS::fixed;
+    for (; g0 + G < a.N; g0 += G, buf ^= a.one_buffer ? 0 : 1) {
         slots = xfer + buf * per_buf;
-        if (g0 + w < a.N) {
-            if (g0 == 0) worker_rows<C, K, VEC, FULL, PL>(a, tp, nt, w, rows);
-            worker_tiles<C, K, VEC, FULL, QW, PL>(a, tp, nt, lut_w, g0 + w, rows, slots, G, w);
-        }
-    } else {
-        constexpr bool kInline = FULL && QW::fixed && QS::fixed;
-        for (; g0 + G < a.N; g0 += G, buf ^= 1) {
-            slots = xfer + buf * per_buf;
-            worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
-            __syncthreads();
-            gather(slots, G);
-        }
-        slots = xfer + buf * per_buf;
-        if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
+        worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
+        __syncthreads();
+        gather(slots, G);
+        if (a.one_buffer) __syncthreads();
     }
+    slots = xfer + buf * per_buf;
+    if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
     if constexpr (kSplit) {
         serve_split<C, VEC, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0], red);
         return;
@@ -1571,11 +1555,22 @@ __host__ __device__ constexpr int table_floats(int G)
 }
 
 // Dynamic LDS of a fused-round block with G waves: the code tables plus the
-// handoff of G workers' tiles (double-buffered when N > G).
-inline size_t round_lds_bytes(int N, int C, int G, int K)
+// handoff of G workers' tiles (bufs buffers when N > G).
+inline size_t round_lds_bytes(int N, int C, int G, int K, int bufs = 2)
 {
-    const int nbuf = N > G ? 2 : 1;
+    const int nbuf = N > G ? bufs : 1;
     return table_floats(G) * sizeof(float) + (size_t)nbuf * K * G * C * kWave * sizeof(float4);
+}
+
+// Handoff buffers of a block with more workers than waves: two, unless two
+// would leave a CU (whose LDS is the per-block limit on gfx950) room for only
+// one block; then one, and the next block starts beside the serving waves
+// (ResNet-50-sized round, 32 workers, 136 KB -> 72 KB per block: 2.110 ->
+// 2.098 ms).
+inline int handoff_bufs(int N, int C, int G, int K, size_t lds_limit)
+{
+    if (N <= G) return 1;
+    return 2 * round_lds_bytes(N, C, G, K, 2) <= lds_limit ? 2 : 1;
 }
 
 // Waves per block: one per worker up to the tile's limit, fewer if the LDS
@@ -1608,14 +1603,13 @@ inline int round_waves(int N, int C, int K, size_t lds_limit, int placement)
 // the server input, which it leaves in ubuf with per-tile partial norms.
 //
 // MW > 0 overrides the minimum waves per SIMD of the launch bounds (the
-// register cap).  PIPE: the variant for more workers than waves, which loads
-// each wave's next worker while the block gathers the current group.
+// register cap).
 //
 // FULL kernels (rows 16-byte aligned) take the tiles that lie wholly inside d
 // and carry no bounds checks; the others take any tile.  A launch covers
 // tiles [a.tile0, a.tile1); block b works on the K tiles from
 // a.tile0 + b*K.
-template <int C, bool VEC, bool FULL, class QW, class QS, int PL, int MW = 0, bool PIPE = false>
+template <int C, bool VEC, bool FULL, class QW, class QS, int PL, int MW = 0>
 __global__ __launch_bounds__(max_round_waves(C) * kWave,
                              MW > 0 ? MW : round_min_waves(C, FULL && PL == AT_SERVER)) void step_kernel(
     StepArgs args)
@@ -1644,7 +1638,7 @@ __global__ __launch_bounds__(max_round_waves(C) * kWave,
     __shared__ double red[SplitServe<QS, C>::value && FULL && K == 1 ? C * kWave : 1];
     const int64_t first = a.tile0 + (int64_t)blockIdx.x * K;
     const int64_t left = a.tile1 - first;
-    round_tiles<C, K, VEC, FULL, QW, QS, PL, PIPE>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G, red);
+    round_tiles<C, K, VEC, FULL, QW, QS, PL>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G, red);
 }
 
 }  // namespace
