@@ -710,10 +710,10 @@ __host__ __device__ constexpr uint32_t dot_weights(int k, int i, bool hi)
 // each group of four bytes into four bits with a shift and a mask; a packed
 // dot product (v_dot4_u32_u8) then weighs the plane bits of a code straight
 // into its byte offset in the code table.
-template <int C, class QT, bool SUM>
+template <int C, class QT, bool SUM, bool SCALED = false>
 __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lut, const CodeWords<C, QT>& w,
                                                   const float (&scs)[C], int64_t base, int nch, int64_t d,
-                                                  uint32_t* stage, float4 (&deq)[C])
+                                                  uint32_t* stage, float4 (&deq)[C], float* stab = nullptr)
 {
     constexpr int R = CodeWords<C, QT>::R;
     constexpr int B = max_code_bits<QT>();
@@ -723,6 +723,17 @@ __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lu
     uint8_t* sb = reinterpret_cast<uint8_t*>(stage);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
+    if constexpr (SCALED) {
+        // One bucket per tile: the wave's own copy of the code table times
+        // the bucket's scale (zero for a gated bucket), one entry per lane,
+        // so each element takes its value in one read; every entry is the
+        // product an element would form itself.
+        static_assert(SUM && (1 << B) <= kWave && QT::cpb(QDev{}) == C, "one scale per tile, small table");
+        const float sc = uniform(scs[0]);
+        const bool ok = !scale_gated<QT>(q) || (sc > 0.0f && !isinf(sc));
+        if (lane < (1 << B)) stab[lane] = (ok ? sc : 0.0f) * lut[lane];
+        lut = stab;
+    }
 #pragma unroll
     for (int ch = 0; ch < C; ++ch)
 #pragma unroll
@@ -773,7 +784,7 @@ __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lu
             const float tv = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(lut) + c4);
             const int kind = QT::kind(q);
             const float s = SUM ? se : sc;
-            const float dv = kind == Q_SCALED_SIGN ? (c4 ? -s : s) : (kind == Q_POW2 ? tv : s * tv);
+            const float dv = SCALED ? tv : kind == Q_SCALED_SIGN ? (c4 ? -s : s) : (kind == Q_POW2 ? tv : s * tv);
             set_comp(deq[ch], k, SUM || (ok && k < nv) ? dv : 0.0f);
         }
     }
@@ -790,17 +801,17 @@ __device__ __forceinline__ void decode_words_rows(const QDev& q, const float* lu
 // stores the lanes past d.  A gated bucket (zero or non-finite scale) then
 // decodes to zeros of either sign, which leave such a sum's bits as +0 would,
 // and the lanes past d or past the tile are not masked: no select per element.
-template <int C, class QT, bool SUM = false>
+template <int C, class QT, bool SUM = false, bool SCALED = false>
 __device__ __forceinline__ void decode_words(const QDev& q, const float* lut, const CodeWords<C, QT>& w,
                                              const float (&scs)[C], int64_t base, int nch, int64_t d,
-                                             uint32_t* stage, float4 (&deq)[C])
+                                             uint32_t* stage, float4 (&deq)[C], float* stab = nullptr)
 {
     // Byte rows for fixed widths of 2 bits and more; 1-bit codes read their
     // four words' halves in one 16-byte read per chunk here, which costs less
     // than writing bytes (ResNet-18-sized sign, 2048-element buckets: 58 against
     // 64 us).
     if constexpr (QT::fixed && max_code_bits<QT>() >= 2) {
-        decode_words_rows<C, QT, SUM>(q, lut, w, scs, base, nch, d, stage, deq);
+        decode_words_rows<C, QT, SUM, SCALED>(q, lut, w, scs, base, nch, d, stage, deq, stab);
         return;
     }
     constexpr int R = CodeWords<C, QT>::R;
@@ -1434,6 +1445,22 @@ __global__ __launch_bounds__(kBlock) void worker_kernel(StepArgs a)
     }
 }
 
+// Whether the aggregate decodes worker messages through a per-wave code
+// table scaled by the bucket's scale: a scaled quantizer fixed at compile
+// time, one bucket per tile, codes of 2 to 6 bits (byte-row decoding, a table
+// of at most 64 entries, one per lane).
+template <class QT, int C>
+__host__ __device__ constexpr bool kScaledTable()
+{
+    if constexpr (QT::fixed) {
+        constexpr QDev q{};
+        return (QT::kind(q) == Q_STOCH || QT::kind(q) == Q_DET) && QT::cpb(q) == C && QT::bits(q) >= 2 &&
+               QT::bits(q) <= 6;
+    } else {
+        return false;
+    }
+}
+
 // Split call: dequantize the N worker messages, average in ascending worker
 // order, run Adam at the server if placed there; result in a.ubuf.  FULL:
 // every tile of the launch lies wholly inside d (no per-tile checks).
@@ -1443,6 +1470,7 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
     static_assert(!FULL || VEC, "whole-tile kernels need aligned rows");
     __shared__ float lut_w[kLutSize];
     __shared__ __attribute__((aligned(16))) uint32_t stage_all[kWavesPerBlock][stage_words<C, QW>()];
+    __shared__ float stab_all[kScaledTable<QW, C>() ? kWavesPerBlock : 1][kWave];
     fill_lut(a.qw, lut_w);
     __syncthreads();
     TilePos t;
@@ -1454,31 +1482,39 @@ __global__ __launch_bounds__(kBlock) void aggregate_kernel(StepArgs a)
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) acc[ch] = zero4();
     // Bit-plane messages: the next worker's code words and scales are loaded
-    // while the current worker's are decoded.
+    // while the current worker's are decoded, into the other of two register
+    // sets, so that each set is waited for only where it is decoded (with one
+    // set copied forward each step, the copy waited for the load at once).
     const bool planes = plane_coded<QW>(a.qw);
-    CodeWords<C, QW> wv;
-    float sc[C];
     if (planes) {
-        load_code_words<C, QW>(a.qw, a.wcodes, t.base, nch, wv);
-        load_chunk_scales<C, QW>(a.qw, a.wscales, t.base, nch, sc);
-    }
-    for (int i = 0; i < a.N; ++i) {
-        if (planes) {
-            const int64_t j = i + 1 < a.N ? i + 1 : i;
-            CodeWords<C, QW> nwv;
-            float nsc[C];
-            load_code_words<C, QW>(a.qw, a.wcodes + j * a.qw.words, t.base, nch, nwv);
-            load_chunk_scales<C, QW>(a.qw, a.wscales + j * a.qw.nscales, t.base, nch, nsc);
-            decode_words<C, QW, true>(a.qw, lut_w, wv, sc, t.base, nch, a.d, stage, dq);
-            wv = nwv;
+        CodeWords<C, QW> wv0, wv1;
+        float sc0[C], sc1[C];
+        const auto load = [&](int64_t i, CodeWords<C, QW>& wv, float (&sc)[C]) {
+            load_code_words<C, QW>(a.qw, a.wcodes + i * a.qw.words, t.base, nch, wv);
+            load_chunk_scales<C, QW>(a.qw, a.wscales + i * a.qw.nscales, t.base, nch, sc);
+        };
+        const auto add = [&](const CodeWords<C, QW>& wv, const float (&sc)[C]) {
+            decode_words<C, QW, true, kScaledTable<QW, C>()>(a.qw, lut_w, wv, sc, t.base, nch, a.d, stage, dq,
+                                                              stab_all[threadIdx.x / kWave]);
 #pragma unroll
-            for (int ch = 0; ch < C; ++ch) sc[ch] = nsc[ch];
-        } else {
+            for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
+        };
+        load(0, wv0, sc0);
+        for (int i = 0; i < a.N; i += 2) {
+            load(i + 1 < a.N ? i + 1 : i, wv1, sc1);
+            add(wv0, sc0);
+            if (i + 1 < a.N) {
+                load(i + 2 < a.N ? i + 2 : i + 1, wv0, sc0);
+                add(wv1, sc1);
+            }
+        }
+    } else {
+        for (int i = 0; i < a.N; ++i) {
             dequant_tile<C, QW>(a.qw, lut_w, a.wcodes + (int64_t)i * a.qw.words,
                                  a.wscales + (int64_t)i * a.qw.nscales, t.base, nch, a.d, stage, dq);
-        }
 #pragma unroll
-        for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
+            for (int ch = 0; ch < C; ++ch) acc[ch] = add4(acc[ch], dq[ch]);
+        }
     }
     // The server's rows load after the decoding: held through it, they cost
     // occupancy (BERT-sized 4-bit, 16 workers: 843 -> 817 us).
