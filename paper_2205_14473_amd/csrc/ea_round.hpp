@@ -166,8 +166,13 @@ __device__ __forceinline__ WordSink message_sink(const QDev& q, uint64_t* codes,
 #ifndef EA_SPARSE_SUBSET
 #define EA_SPARSE_SUBSET 3
 #endif
+// Tiles of 4 and 8 chunks: 8 keys per lane, so the first search covers k <=
+// 128 (BERT-sized round, top-128 of 2048: 9.19 -> 7.35 ms against 5 keys per
+// lane; top-64 of 2048 6.92 -> 7.13, random-64 of 2048 7.57 -> 7.63, top-100
+// of 1024 unchanged).  Choosing 5 or 8 per bucket from k kept both gains on
+// paper but the second search path slowed the first (top-64 7.19 ms).
 #ifndef EA_SPARSE_SUBSET_WIDE
-#define EA_SPARSE_SUBSET_WIDE 5
+#define EA_SPARSE_SUBSET_WIDE 8
 #endif
 __host__ __device__ constexpr int sparse_subset(int C)
 {
@@ -245,7 +250,7 @@ __device__ __forceinline__ void wave_or_and(uint32_t vo, uint32_t va, uint32_t& 
 // the bits those keys all share (for magnitudes, typically the sign and most
 // of the exponent); r runs up to S below.  (2)
 // For k <= 16 S it first runs on each lane's S largest keys only (S ballots a
-// step instead of 4 per chunk; S = 3 for tiles of up to 2 chunks, 5 for wider
+// step instead of 4 per chunk; S = 3 for tiles of up to 2 chunks, 8 for wider
 // ones) and keeps that answer when a full count confirms it; else it runs
 // again over every key.  A lane then holds k/64 <= S/4 of the k largest keys
 // on average, so few buckets have a lane with more than S of them; for larger
