@@ -208,6 +208,18 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
 hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
                             size_t limit, hipStream_t s);
 
+// Waves per block of a fused-round launch: one per worker up to the tile's
+// limit.  Fully specialized wide tiles serve a whole-tile server bucket on C
+// waves, one chunk each (SplitServe, whole and ragged tiles alike), so their
+// blocks have C waves at least.
+int step_waves(const StepArgs& a, int C, int K, const Special* sp, const SymKernel* sk, size_t limit)
+{
+    const int G = round_waves(a.N, C, K, limit, a.placement);
+    const bool split = (sp || sk) && C == 8 && a.qs.cpb == C &&
+                       (a.qs.kind == Q_SCALED_SIGN || a.qs.kind == Q_STOCH || a.qs.kind == Q_DET);
+    return split && G < C ? C : G;
+}
+
 // Tiles per block of the whole-tile launch.
 int main_tiles_per_block(int C, const Special* sp, const SymKernel* sk, const HalfKernel* hk)
 {
@@ -319,12 +331,7 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
                             const HalfKernel* hk, size_t limit, hipStream_t s)
 {
     const int K = main_tiles_per_block(C, sp, sk, hk);
-    int G = round_waves(a.N, C, K, limit, a.placement);
-    // fully specialized wide tiles serve the whole-tile server bucket on C
-    // waves, one chunk each (SplitServe), so their blocks have C waves at least
-    const bool split = (sp || sk) && C == 8 && a.qs.cpb == C &&
-                       (a.qs.kind == Q_SCALED_SIGN || a.qs.kind == Q_STOCH || a.qs.kind == Q_DET);
-    if (split && G < C) G = C;
+    const int G = step_waves(a, C, K, sp, sk, limit);
     StepArgs b = a;
     b.tile0 = 0;
     b.tile1 = nfull;
@@ -356,7 +363,7 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
 hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
                             size_t limit, hipStream_t s)
 {
-    const int G = round_waves(a.N, C, 1, limit, a.placement);
+    const int G = step_waves(a, C, 1, sp, sk, limit);
     StepArgs b = a;
     b.tile0 = nfull;
     b.tile1 = a.ntiles;

@@ -1254,36 +1254,38 @@ __device__ __forceinline__ void gather_chunk(const float4* slot, int cnt, int ch
     for (int j = 0; j < cnt; ++j) acc = add4(acc, slot[(j * C + ch) * kWave + lane]);
 }
 
-// The server side of one whole tile on C waves: wave ch gathers chunk ch of
-// the last group, runs Adam (at the server) and adds e_s on it; the lane
-// partials of the bucket norm meet in `red` ([C][64], LDS) and every serving
-// wave adds them in chunk order (the order of the one-wave round, so the
-// scale has the same bits), then quantizes its chunk under that scale and
-// applies it.  Every wave of the block takes part in both barriers.
-template <int C, bool VEC, class QS, int PL>
+// The server side of one tile on C waves: wave ch gathers chunk ch of the
+// last group, runs Adam (at the server) and adds e_s on it; the lane partials
+// of the bucket norm meet in `red` ([C][64], LDS) and every serving wave adds
+// them in chunk order (the order of the one-wave round, so the scale has the
+// same bits), then quantizes its chunk under that scale and applies it.
+// Every wave of the block takes part in both barriers.  FULL = false: a
+// ragged tile, served on the waves of its nch chunks, with bounds checks.
+template <int C, bool VEC, bool FULL, class QS, int PL>
 __device__ __forceinline__ void serve_split(const StepArgs& a, const TilePos& t, const float* lut_s,
                                             const float4* slots, int cnt, float4 acc, double* red)
 {
     using QG = typename GivenScale<QS>::type;
     const int lane = lane_id();
     const int w = (int)(threadIdx.x / kWave);
-    const bool serving = w < C;
+    const int nch = FULL ? C : t.nch;
+    const bool serving = w < nch;
     const int ch = serving ? w : 0;
     const int64_t base = t.base + (int64_t)ch * kChunk;
     const int norm = QS::norm(a.qs);
     ServerRows<1> sr;
-    if (serving) load_server<1, VEC, true, PL>(a, base, 1, true, true, sr);
+    if (serving) load_server<1, VEC, FULL, PL>(a, base, 1, true, true, sr);
     __syncthreads();                           // the last group's handoff is complete
     float4 u[1], q[1], dq[1];
     if (serving) {
         gather_chunk<C>(slots, cnt, ch, acc);
         const float4 s1[1] = {acc};
-        server_input<1, VEC, true, PL>(a, s1, base, 1, sr, u);
+        server_input<1, VEC, FULL, PL>(a, s1, base, 1, sr, u);
         q[0] = add4(u[0], sr.e[0]);
         Partial p;
         p.sum = 0.0;
         p.mx = 0.0f;
-        partial_add4(p, norm, q[0], 4);
+        partial_add4(p, norm, q[0], FULL ? 4 : nvalid4(base + 4 * lane, a.d));
         red[ch * kWave + lane] = norm == S_MAX ? (double)p.mx : p.sum;
     }
     __syncthreads();                           // every chunk's partial is in LDS
@@ -1292,20 +1294,22 @@ __device__ __forceinline__ void serve_split(const StepArgs& a, const TilePos& t,
     float mx = 0.0f;
 #pragma unroll
     for (int j = 0; j < C; ++j) {
+        if (!FULL && j >= nch) continue;
         if (norm == S_MAX) mx = fmaxf(mx, (float)red[j * kWave + lane]);
         else tot += red[j * kWave + lane];
     }
     const double S = norm == S_MAX ? 0.0 : wave_sum(tot);
     const float M = norm == S_MAX ? wave_max(mx) : 0.0f;
-    const float scale = scale_from(norm, S, M, a.qs.B);
+    const int64_t nb = FULL ? a.qs.B : ((a.d - t.base) < a.qs.B ? (a.d - t.base) : a.qs.B);
+    const float scale = scale_from(norm, S, M, nb);
     if (ch == 0 && lane == 0) a.sscales[(t.base >> 8) >> QS::cpb_shift(a.qs)] = scale;
     WordSink sink = message_sink<QG>(a.qs, a.scodes, base);
-    quantize_tile<1, true, QG>(a.qs, lut_s, q, base, 1, a.d, a.k0, a.k1, a.t, kServerStream, scale, a.scodes,
+    quantize_tile<1, FULL, QG>(a.qs, lut_s, q, base, 1, a.d, a.k0, a.k1, a.t, kServerStream, scale, a.scodes,
                                a.sscales, sink, dq);
     sink.flush();
     const int64_t n = base + 4 * lane;
-    st4<VEC, true>(a.e_s, n, a.d, a.qs.ef ? sub4(q[0], dq[0]) : zero4());
-    st4<VEC, true>(a.x, n, a.d, sub4(sr.x[0], dq[0]));
+    st4<VEC, FULL>(a.e_s, n, a.d, a.qs.ef ? sub4(q[0], dq[0]) : zero4());
+    st4<VEC, FULL>(a.x, n, a.d, sub4(sr.x[0], dq[0]));
 }
 
 // ---------------------------------------------------------------------------
@@ -1334,7 +1338,7 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
     const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
     // The server side on C waves, one chunk each (the launch gives the block
     // at least C waves); otherwise wave k serves tile k.
-    constexpr bool kSplit = SplitServe<QS, C>::value && FULL && K == 1;
+    constexpr bool kSplit = SplitServe<QS, C>::value && K == 1;
     // Whole-tile launches give every block exactly K tiles.  With that known
     // at compile time, each wave's loads of all K tiles and its work on them
     // are straight-line code, so the compiler waits for each tile's rows
@@ -1378,7 +1382,7 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
     slots = xfer + buf * per_buf;
     if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
     if constexpr (kSplit) {
-        serve_split<C, VEC, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0], red);
+        serve_split<C, VEC, FULL, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0], red);
         return;
     } else {
     const TilePos t = tile_at<C>(a, tile0 + (w < nt ? w : 0));
@@ -1676,7 +1680,7 @@ __global__ __launch_bounds__(max_round_waves(C) * kWave,
     }
     float4* xfer = smem + table_floats(G) / 4;
     constexpr int K = kernel_tiles(C, FULL, PL, half_kernel<QW, QS, PL>());
-    __shared__ double red[SplitServe<QS, C>::value && FULL && K == 1 ? C * kWave : 1];
+    __shared__ double red[SplitServe<QS, C>::value && K == 1 ? C * kWave : 1];
     const int64_t first = a.tile0 + (int64_t)blockIdx.x * K;
     const int64_t left = a.tile1 - first;
     round_tiles<C, K, VEC, FULL, QW, QS, PL>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G, red);
