@@ -209,14 +209,17 @@ hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Speci
                             size_t limit, hipStream_t s);
 
 // Waves per block of a fused-round launch: one per worker up to the tile's
-// limit.  Fully specialized wide tiles serve a whole-tile server bucket on C
-// waves, one chunk each (SplitServe, whole and ragged tiles alike), so their
-// blocks have C waves at least.
+// limit.  Fully specialized 8-chunk tiles serve a whole-tile server bucket,
+// or a sparsifier's server side, on C waves, one chunk each (SplitServe,
+// SparseServe; whole and ragged tiles alike), so their blocks have C waves
+// at least.
 int step_waves(const StepArgs& a, int C, int K, const Special* sp, const SymKernel* sk, size_t limit)
 {
     const int G = round_waves(a.N, C, K, limit, a.placement);
-    const bool split = (sp || sk) && C == 8 && a.qs.cpb == C &&
-                       (a.qs.kind == Q_SCALED_SIGN || a.qs.kind == Q_STOCH || a.qs.kind == Q_DET);
+    const bool scaled = a.qs.cpb == C &&
+                        (a.qs.kind == Q_SCALED_SIGN || a.qs.kind == Q_STOCH || a.qs.kind == Q_DET);
+    const bool sparse = a.qs.kind == Q_TOPK || a.qs.kind == Q_RANDK;
+    const bool split = (sp || sk) && C == 8 && (scaled || sparse);
     return split && G < C ? C : G;
 }
 

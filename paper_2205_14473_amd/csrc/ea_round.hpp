@@ -189,24 +189,27 @@ __host__ __device__ constexpr int sparse_subset(int C)
 // candidate is reached by exactly kk values, that candidate with exact set.
 // Each step is one ballot per counted value slot; the loop is kept rolled
 // (unrolling it measured no faster and multiplies the code).
+struct Selected {
+    uint32_t T;
+    bool exact;
+};
 template <class Count>
-__device__ __forceinline__ uint32_t bit_select(const Count& count, uint32_t kk, int top, uint32_t T0, bool& exact)
+__device__ __forceinline__ Selected bit_select(const Count& count, uint32_t kk, int top, uint32_t T0)
 {
-    uint32_t T = T0;
-    exact = false;
+    Selected r{T0, false};
 #pragma nounroll
     for (int bit = top; bit >= 0; --bit) {
-        const uint32_t cand = T | (1u << bit);
+        const uint32_t cand = r.T | (1u << bit);
         const uint32_t n = count(cand);
         if (n >= kk) {
-            T = cand;
+            r.T = cand;
             if (n == kk) {
-                exact = true;
+                r.exact = true;
                 break;
             }
         }
     }
-    return T;
+    return r;
 }
 
 __device__ __forceinline__ uint32_t wave_count(bool pred)
@@ -273,24 +276,41 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
     const int top = topk ? 31 : 23;   // keys below 2^31 (TOPK) or 2^24 (RANDK)
     if (FULL) nch = C;
 
-    uint32_t key[C][4];
+    // On tiles of 4 or more chunks a top-k key fixed at compile time is
+    // formed from p where it is used (one AND), so the tile's keys take no
+    // registers of their own.  (On narrower tiles registers are not short,
+    // and held keys measured faster.)
+    constexpr bool kKeyOfP = C >= 4 && QT::fixed && QT::kind(QDev{}) == Q_TOPK;
+    uint32_t keys[kKeyOfP ? 1 : C][4];
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
-        const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
-        const int nv = FULL ? 4 : (ch < nch ? nvalid4(n, d) : 0);
-        uint4 r = make_uint4(0u, 0u, 0u, 0u);
-        if (!topk && (FULL || ch < nch)) {
-            const uint64_t j = (uint64_t)n >> 2;
-            r = philox10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), step, sid), k0, k1);
-        }
-        const uint32_t rr[4] = {r.x, r.y, r.z, r.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const uint32_t kv = topk ? (__float_as_uint(comp(p[ch], k)) & 0x7FFFFFFFu) : (rr[k] >> 8);
-            key[ch][k] = (FULL || k < nv) ? kv : 0u;
-        }
         deq[ch] = zero4();
+        if constexpr (!kKeyOfP) {
+            const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
+            const int nv = FULL ? 4 : (ch < nch ? nvalid4(n, d) : 0);
+            uint4 r = make_uint4(0u, 0u, 0u, 0u);
+            if (!topk && (FULL || ch < nch)) {
+                const uint64_t j = (uint64_t)n >> 2;
+                r = philox10(make_uint4((uint32_t)j, (uint32_t)(j >> 32), step, sid), k0, k1);
+            }
+            const uint32_t rr[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t kv = topk ? (__float_as_uint(comp(p[ch], k)) & 0x7FFFFFFFu) : (rr[k] >> 8);
+                keys[ch][k] = (FULL || k < nv) ? kv : 0u;
+            }
+        }
     }
+    const auto key = [&](int j, int k) -> uint32_t {
+        if constexpr (kKeyOfP) {
+            uint32_t kv;
+            asm volatile("v_and_b32 %0, 0x7fffffff, %1" : "=v"(kv) : "v"(comp(p[j], k)));
+            if constexpr (FULL) return kv;
+            else return j < nch && k < nvalid4(base + (int64_t)j * kChunk + 4 * lane, d) ? kv : 0u;
+        } else {
+            return keys[j][k];
+        }
+    };
 
     const int64_t chunk0 = base >> 8;
 #pragma unroll
@@ -308,7 +328,7 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
             for (int j = 0; j < C; ++j) {
                 if (j < b0 || j >= b0 + cpb) continue;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) n += wave_count(key[j][k] >= c);
+                for (int k = 0; k < 4; ++k) n += wave_count(key(j, k) >= c);
             }
             return n;
         };
@@ -324,7 +344,7 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
             if (j < b0 || j >= b0 + cpb) continue;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                const uint32_t x = key[j][k];
+                const uint32_t x = key(j, k);
 #pragma unroll
                 for (int r = (S > 0 ? S : 1) - 1; r > 0; --r) m[r] = max(m[r], min(m[r - 1], x));
                 m[0] = max(m[0], x);
@@ -364,9 +384,9 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
                 for (int r = 0; r < S; ++r) n += wave_count(m[r] >= c);
                 return n;
             };
-            bool er;
-            const uint32_t Tr = bit_select(count_sub, kk, hi, prefix, er);
-            if (er) {
+            const Selected sr = bit_select(count_sub, kk, hi, prefix);
+            const uint32_t Tr = sr.T;
+            if (sr.exact) {
                 found = exact = count_all(Tr) == kk;
             } else {
                 gt = count_all(Tr + 1u);
@@ -374,18 +394,15 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
             }
             T = Tr;
         }
-        if (!found) T = bit_select(count_all, kk, hi, prefix, exact);
+        if (!found) {
+            const Selected sa = bit_select(count_all, kk, hi, prefix);
+            T = sa.T;
+            exact = sa.exact;
+        }
 
-        // Kept flags, bit 4j + k of a lane for its element in chunk j, slot k.
-        uint32_t kbits = 0u;
-        if (exact) {
-#pragma unroll
-            for (int j = 0; j < C; ++j) {
-                if (j < b0 || j >= b0 + cpb) continue;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) kbits |= (key[j][k] >= T ? 1u : 0u) << (4 * j + k);
-            }
-        } else {
+        // Keys equal to T are kept in element order until kk are kept in all:
+        // need of them after the gt keys above T.
+        const auto need_of = [&]() {
             if (!have_gt) {
                 gt = 0u;
 #pragma unroll
@@ -393,61 +410,132 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
                     if (j < b0 || j >= b0 + cpb) continue;
 #pragma unroll
                     for (int k = 0; k < 4; ++k)
-                        gt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key[j][k] > T));
+                        gt += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(key(j, k) > T));
                 }
             }
-            const uint32_t need = kk - gt;
+            return kk - gt;
+        };
+
+        // Then the kept flags, the code words, the values in element order
+        // and the dequantized tile.  A plain store for the values: the caches
+        // merge the bucket's scattered 4-byte stores.
+        float* vb = vals + ((chunk0 + b0) >> QT::cpb_shift(q)) * (int64_t)q.keep;
+        if constexpr (C <= 2) {
+            // Kept flags first, bit 4j + k of a lane for its element in chunk
+            // j, slot k; then the rest.  (For wider tiles the flag word takes
+            // a register per bit constant past 64.)
+            uint32_t kbits = 0u;
+            if (exact) {
+#pragma unroll
+                for (int j = 0; j < C; ++j) {
+                    if (j < b0 || j >= b0 + cpb) continue;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) kbits |= (key(j, k) >= T ? 1u : 0u) << (4 * j + k);
+                }
+            } else {
+                const uint32_t need = need_of();
+                uint32_t before = 0;
+#pragma unroll
+                for (int j = 0; j < C; ++j) {
+                    if (j < b0 || j >= b0 + cpb) continue;
+                    uint32_t below = 0, tot = 0;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const uint64_t em = __builtin_amdgcn_ballot_w64(key(j, k) == T);
+                        below += lanes_below(em);
+                        tot += (uint32_t)__builtin_popcountll(em);
+                    }
+                    uint32_t own = 0;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const bool eq = key(j, k) == T;
+                        const bool kept = key(j, k) > T || (eq && before + below + own < need);
+                        kbits |= (kept ? 1u : 0u) << (4 * j + k);
+                        own += eq ? 1u : 0u;
+                    }
+                    before += tot;
+                }
+            }
             uint32_t before = 0;
 #pragma unroll
             for (int j = 0; j < C; ++j) {
                 if (j < b0 || j >= b0 + cpb) continue;
+                if (!FULL && j >= nch) continue;
+                uint64_t km[4];
                 uint32_t below = 0, tot = 0;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    const uint64_t em = __builtin_amdgcn_ballot_w64(key[j][k] == T);
-                    below += lanes_below(em);
-                    tot += (uint32_t)__builtin_popcountll(em);
+                    km[k] = __builtin_amdgcn_ballot_w64(((kbits >> (4 * j + k)) & 1u) != 0u);
+                    below += lanes_below(km[k]);
+                    tot += (uint32_t)__builtin_popcountll(km[k]);
                 }
                 uint32_t own = 0;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    const bool eq = key[j][k] == T;
-                    const bool kept = key[j][k] > T || (eq && before + below + own < need);
-                    kbits |= (kept ? 1u : 0u) << (4 * j + k);
-                    own += eq ? 1u : 0u;
+                    const bool kept = ((kbits >> (4 * j + k)) & 1u) != 0u;
+                    const float x = comp(p[j], k);
+                    const uint32_t pos = before + below + own;   // < kk by construction; guarded all the same
+                    if (kept && pos < (uint32_t)q.keep) vb[pos] = x;
+                    own += kept ? 1u : 0u;
+                    set_comp(deq[j], k, kept ? x : 0.0f);
+                    sink.put(km[k]);
                 }
                 before += tot;
             }
-        }
-
-        // Code words, values in element order, and the dequantized tile.  A
-        // plain store: the caches merge the bucket's scattered 4-byte values.
-        float* vb = vals + ((chunk0 + b0) >> QT::cpb_shift(q)) * (int64_t)q.keep;
-        uint32_t before = 0;
+        } else {
+            // Chunk by chunk, each chunk's flags just before its output (the
+            // same steps; the output loop is written out in both branches
+            // because sharing it measured slower on these tiles: random-64 of
+            // 2048 5.7 -> 6.4 ms).  Chunks past d come last in element
+            // order, so skipping them leaves the ranks of the others as they
+            // are.
+            const uint32_t need = exact ? 0u : need_of();
+            uint32_t eq_before = 0, kept_before = 0;
 #pragma unroll
-        for (int j = 0; j < C; ++j) {
-            if (j < b0 || j >= b0 + cpb) continue;
-            if (!FULL && j >= nch) continue;
-            uint64_t km[4];
-            uint32_t below = 0, tot = 0;
+            for (int j = 0; j < C; ++j) {
+                if (j < b0 || j >= b0 + cpb) continue;
+                if (!FULL && j >= nch) continue;
+                bool kept[4];
+                if (exact) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                km[k] = __builtin_amdgcn_ballot_w64(((kbits >> (4 * j + k)) & 1u) != 0u);
-                below += lanes_below(km[k]);
-                tot += (uint32_t)__builtin_popcountll(km[k]);
+                    for (int k = 0; k < 4; ++k) kept[k] = key(j, k) >= T;
+                } else {
+                    uint32_t below = 0, tot = 0;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const uint64_t em = __builtin_amdgcn_ballot_w64(key(j, k) == T);
+                        below += lanes_below(em);
+                        tot += (uint32_t)__builtin_popcountll(em);
+                    }
+                    uint32_t own = 0;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const bool eq = key(j, k) == T;
+                        kept[k] = key(j, k) > T || (eq && eq_before + below + own < need);
+                        own += eq ? 1u : 0u;
+                    }
+                    eq_before += tot;
+                }
+                uint64_t km[4];
+                uint32_t below = 0, tot = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    km[k] = __builtin_amdgcn_ballot_w64(kept[k]);
+                    below += lanes_below(km[k]);
+                    tot += (uint32_t)__builtin_popcountll(km[k]);
+                }
+                uint32_t own = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float x = comp(p[j], k);
+                    const uint32_t pos = kept_before + below + own;   // < kk by construction; guarded all the same
+                    if (kept[k] && pos < (uint32_t)q.keep) vb[pos] = x;
+                    own += kept[k] ? 1u : 0u;
+                    set_comp(deq[j], k, kept[k] ? x : 0.0f);
+                    sink.put(km[k]);
+                }
+                kept_before += tot;
             }
-            uint32_t own = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const bool kept = ((kbits >> (4 * j + k)) & 1u) != 0u;
-                const float x = comp(p[j], k);
-                const uint32_t pos = before + below + own;   // < kk by construction; guarded all the same
-                if (kept && pos < (uint32_t)q.keep) vb[pos] = x;
-                own += kept ? 1u : 0u;
-                set_comp(deq[j], k, kept ? x : 0.0f);
-                sink.put(km[k]);
-            }
-            before += tot;
         }
         // A bucket shorter than keep: the remaining value slots are zero.
         if (!FULL)
@@ -1312,6 +1400,65 @@ __device__ __forceinline__ void serve_split(const StepArgs& a, const TilePos& t,
     st4<VEC, FULL>(a.x, n, a.d, sub4(sr.x[0], dq[0]));
 }
 
+// 8-chunk tiles with a sparsifier on the server (top-k, random-k): the
+// server's Adam runs on 8 waves, one chunk each, and one wave then selects
+// and codes the whole tile (the threshold search needs every key of a
+// bucket).  No wave holds all eight chunks' server rows, which kept these
+// kernels at two waves per SIMD.
+template <class QT, int C>
+struct SparseServe {
+    static constexpr bool value = false;
+};
+template <int K, int B, int NM, int CPB, int C>
+struct SparseServe<QCt<K, B, NM, CPB>, C> {
+    static constexpr bool value = C == 8 && (K == Q_TOPK || K == Q_RANDK);
+};
+
+// The server side of one tile for SparseServe: wave ch gathers chunk ch of
+// the last group, runs Adam on it and adds e_s; it leaves q and x in the
+// handoff slots of workers 0 and 1 of chunk ch, which no other wave reads.
+// Wave 0 then sparsifies the tile's q and writes e_s and x.  Every wave of
+// the block takes part in both barriers.  FULL = false: a ragged tile, with
+// bounds checks.
+template <int C, bool VEC, bool FULL, class QS, int PL>
+__device__ __forceinline__ void serve_sparse(const StepArgs& a, const TilePos& t, const float* lut_s,
+                                             float4* slots, int cnt, float4 acc)
+{
+    const int lane = lane_id();
+    const int w = (int)(threadIdx.x / kWave);
+    const int nch = FULL ? C : t.nch;
+    const bool serving = w < nch;
+    const int ch = serving ? w : 0;
+    const int64_t base = t.base + (int64_t)ch * kChunk;
+    ServerRows<1> sr;
+    if (serving) load_server<1, VEC, FULL, PL>(a, base, 1, true, true, sr);
+    __syncthreads();                           // the last group's handoff is complete
+    if (serving) {
+        gather_chunk<C>(slots, cnt, ch, acc);
+        const float4 s1[1] = {acc};
+        float4 u[1];
+        server_input<1, VEC, FULL, PL>(a, s1, base, 1, sr, u);
+        slots[ch * kWave + lane] = add4(u[0], sr.e[0]);
+        slots[(C + ch) * kWave + lane] = sr.x[0];
+    }
+    __syncthreads();                           // q and x of every chunk are in LDS
+    if (w != 0) return;
+    float4 q[C], dq[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) q[j] = (FULL || j < nch) ? slots[j * kWave + lane] : zero4();
+    WordSink sink = message_sink<QS>(a.qs, a.scodes, t.base);
+    quantize_tile<C, FULL, QS>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, 0.0f, a.scodes,
+                               a.sscales, sink, dq);
+    sink.flush();
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+        if (!FULL && j >= nch) continue;
+        const int64_t n = t.base + (int64_t)j * kChunk + 4 * lane;
+        st4<VEC, FULL>(a.e_s, n, a.d, a.qs.ef ? sub4(q[j], dq[j]) : zero4());
+        st4<VEC, FULL>(a.x, n, a.d, sub4(slots[(C + j) * kWave + lane], dq[j]));
+    }
+}
+
 // ---------------------------------------------------------------------------
 // The fused round on nt <= K consecutive tiles per block.  The block has
 // G = min(N, 16) waves.  Workers are taken in groups of G: wave w compresses
@@ -1338,7 +1485,8 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
     const bool sglobal = has_scale<QS>(a.qs) && QS::cpb(a.qs) == 0;
     // The server side on C waves, one chunk each (the launch gives the block
     // at least C waves); otherwise wave k serves tile k.
-    constexpr bool kSplit = SplitServe<QS, C>::value && K == 1;
+    constexpr bool kSparse = SparseServe<QS, C>::value && K == 1;
+    constexpr bool kSplit = (SplitServe<QS, C>::value || kSparse) && K == 1;
     // Whole-tile launches give every block exactly K tiles.  With that known
     // at compile time, each wave's loads of all K tiles and its work on them
     // are straight-line code, so the compiler waits for each tile's rows
@@ -1382,7 +1530,8 @@ __device__ __forceinline__ void round_tiles(const StepArgs& a, int64_t tile0, in
     slots = xfer + buf * per_buf;
     if (g0 + w < a.N) worker_round<C, K, VEC, FULL, QW, PL, kInline>(a, tp, nt, lut_w, g0 + w, slots, G, w);
     if constexpr (kSplit) {
-        serve_split<C, VEC, FULL, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0], red);
+        if constexpr (kSparse) serve_sparse<C, VEC, FULL, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0]);
+        else serve_split<C, VEC, FULL, QS, PL>(a, tp[0], lut_s, slots, a.N - g0, acc[0], red);
         return;
     } else {
     const TilePos t = tile_at<C>(a, tile0 + (w < nt ? w : 0));

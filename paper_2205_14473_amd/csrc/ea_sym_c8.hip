@@ -16,12 +16,20 @@ namespace {
 #ifndef EA_SYM_C8_MIN_WAVES
 #define EA_SYM_C8_MIN_WAVES 2
 #endif
+// The sparsifiers' whole-tile kernels serve on eight waves and select on one
+// (SparseServe), and fit in fewer registers.
+#ifndef EA_SYM_C8_TOPK_MIN_WAVES
+#define EA_SYM_C8_TOPK_MIN_WAVES 4
+#endif
+#ifndef EA_SYM_C8_RANDK_MIN_WAVES
+#define EA_SYM_C8_RANDK_MIN_WAVES 3
+#endif
 
-template <class Q>
+template <class Q, int MW = EA_SYM_C8_MIN_WAVES>
 constexpr SymKernel sym()
 {
     return SymKernel{8, Q::kind(QDev{}), Q::bits(QDev{}), Q::norm(QDev{}), Q::cpb(QDev{}),
-                     step_kernel<8, true, true, Q, Q, AT_SERVER, EA_SYM_C8_MIN_WAVES>,
+                     step_kernel<8, true, true, Q, Q, AT_SERVER, MW>,
                      round_tiles_per_block(8, true), step_kernel<8, true, false, Q, Q, AT_SERVER, EA_SYM_C8_MIN_WAVES>};
 }
 
@@ -35,8 +43,8 @@ const SymKernel kSym[] = {
     sym<QCt<Q_STOCH, 4, S_MAX, 8>>(),
     sym<QCt<Q_STOCH, 8, S_L2, 8>>(),
     sym<QCt<Q_STOCH, 8, S_MAX, 8>>(),
-    sym<QCt<Q_TOPK, 1, S_MAX, 8>>(),
-    sym<QCt<Q_RANDK, 1, S_MAX, 8>>(),
+    sym<QCt<Q_TOPK, 1, S_MAX, 8>, EA_SYM_C8_TOPK_MIN_WAVES>(),
+    sym<QCt<Q_RANDK, 1, S_MAX, 8>, EA_SYM_C8_RANDK_MIN_WAVES>(),
 };
 
 }  // namespace

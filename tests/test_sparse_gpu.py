@@ -73,6 +73,19 @@ def test_generic_kernels(kind, bucket, keep, placement):
 
 
 @pytest.mark.parametrize("kind", list(SPARSE))
+@pytest.mark.parametrize("d,N,keep", [(2048 * 9 + 700, 16, 128), (2048 * 5, 11, 64), (2048 * 4 + 1030, 20, 300),
+                                      (2048 * 3 + 2047, 8, 2048)])
+def test_wide_tile_kernels(kind, d, N, keep):
+    """Bucket 2048 on both sides with Adam at the server: the fully
+    specialized 8-chunk kernels, whose server side runs Adam on eight waves,
+    one chunk each, and selects on one of them.  Several worker groups (the
+    last one partial with 11 and 20 workers), ragged tails, keep within and
+    past the first search's range, and keep = bucket."""
+    q = SPARSE[kind](keep, 2048)
+    _run(d, N, q, q, O.ADAM_AT_SERVER, T=3, seed=keep)
+
+
+@pytest.mark.parametrize("kind", list(SPARSE))
 def test_split_calls(kind):
     q = SPARSE[kind](24, 512)
     _run(512 * 9 + 130, 5, q, q, O.ADAM_AT_SERVER, T=4, split=True)
