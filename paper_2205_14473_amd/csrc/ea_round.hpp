@@ -1055,15 +1055,66 @@ __device__ __forceinline__ void load_worker(const StepArgs& a, const float* __re
     }
 }
 
+// Adam's step lr * (m / sqrt(v)) (0 where v <= 0) on n values per lane, the
+// square root and the division correctly rounded.  When every lane's values
+// have v in [2^-96, 2^96] and |m| in [2^-60, 2^40] (a wave-uniform test),
+// the square root needs no prescale and no special-value fixup, and the
+// division no operand scaling and no fixup (the quotient and its operands
+// stay normal and far from overflow), so each is computed from the hardware
+// estimate and the same exact correction steps alone: the rounded square
+// root is picked among s and its two neighbours by the signs of the fma
+// residuals v - s'*s, and the quotient is refined from the reciprocal by
+// fma residuals.  The results equal those of sqrtf and '/'; any other wave
+// takes those.
+template <int n>
+__device__ __forceinline__ void adam_step(const float (&m)[n], const float (&v)[n], float lr, float (&u)[n])
+{
+    uint32_t vlo = 0xFFFFFFFFu, vhi = 0u;
+    float mlo = __builtin_inff(), mhi = 0.0f;
+#pragma unroll
+    for (int i = 0; i < n; ++i) {
+        vlo = min(vlo, __float_as_uint(v[i]));
+        vhi = max(vhi, __float_as_uint(v[i]));
+        mlo = fminf(mlo, fabsf(m[i]));
+        mhi = fmaxf(mhi, fabsf(m[i]));
+    }
+    // v >= 0 by construction; a NaN or negative v (bit pattern above 2^96)
+    // fails the test, and so does a NaN or infinite m, which makes v NaN or
+    // infinite as well
+    const bool ok = vlo >= 0x0F800000u && vhi <= 0x6F800000u && mlo >= 0x1p-60f && mhi <= 0x1p40f;
+    if (__builtin_amdgcn_ballot_w64(!ok) == 0) {
+#pragma unroll
+        for (int i = 0; i < n; ++i) {
+            float s = __builtin_amdgcn_sqrtf(v[i]);
+            const float sdn = __uint_as_float(__float_as_uint(s) - 1u);
+            const float sup = __uint_as_float(__float_as_uint(s) + 1u);
+            const float rdn = fmaf(-sdn, s, v[i]);
+            const float rup = fmaf(-sup, s, v[i]);
+            s = rdn <= 0.0f ? sdn : s;
+            s = rup > 0.0f ? sup : s;
+            float r = __builtin_amdgcn_rcpf(s);
+            r = fmaf(fmaf(-s, r, 1.0f), r, r);
+            float q = m[i] * r;
+            q = fmaf(fmaf(-s, q, m[i]), r, q);
+            q = fmaf(fmaf(-s, q, m[i]), r, q);
+            u[i] = lr * q;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < n; ++i) u[i] = v[i] > 0.0f ? lr * (m[i] / sqrtf(v[i])) : 0.0f;
+    }
+}
+
 // p for a worker: g + e (Adam at the server) or lr*m/sqrt(v) + e after the
 // moment update (Adam at the workers); updated moments are left in r.
 template <int C, int PL>
 __device__ __forceinline__ void worker_p(const StepArgs& a, WorkerRows<C>& r, float4 (&p)[C])
 {
     const float omb1 = 1.0f - a.beta1, omb2 = 1.0f - a.beta2;
+    if (placement_of<PL>(a) == AT_WORKER) {
+        float mm[4 * C], vv[4 * C], uu[4 * C];
 #pragma unroll
-    for (int ch = 0; ch < C; ++ch) {
-        if (placement_of<PL>(a) == AT_WORKER) {
+        for (int ch = 0; ch < C; ++ch) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const float gk = comp(r.g[ch], k);
@@ -1071,12 +1122,19 @@ __device__ __forceinline__ void worker_p(const StepArgs& a, WorkerRows<C>& r, fl
                 const float mk = a.beta1 * comp(r.m[ch], k) + omb1 * gk;
                 set_comp(r.v[ch], k, vk);
                 set_comp(r.m[ch], k, mk);
-                const float uk = vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f;
-                set_comp(p[ch], k, uk + comp(r.e[ch], k));
+                mm[4 * ch + k] = mk;
+                vv[4 * ch + k] = vk;
             }
-        } else {
-            p[ch] = add4(r.g[ch], r.e[ch]);
         }
+        adam_step<4 * C>(mm, vv, a.lr, uu);
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) set_comp(p[ch], k, uu[4 * ch + k] + comp(r.e[ch], k));
+        }
+    } else {
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) p[ch] = add4(r.g[ch], r.e[ch]);
     }
 }
 
@@ -1138,6 +1196,34 @@ __device__ __forceinline__ void server_input(const StepArgs& a, const float4 (&a
     const bool pow2 = (a.N & (a.N - 1)) == 0;
     const float invN = 1.0f / fN;
     const float omb1 = 1.0f - a.beta1, omb2 = 1.0f - a.beta2;
+    float4 avg[C];
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch)
+        avg[ch] = make_float4(avg_of(acc[ch].x, fN, invN, pow2), avg_of(acc[ch].y, fN, invN, pow2),
+                              avg_of(acc[ch].z, fN, invN, pow2), avg_of(acc[ch].w, fN, invN, pow2));
+    if (placement_of<PL>(a) == AT_SERVER) {
+        // the moments of every chunk (those past d are zero and unused)
+        float mm[4 * C], vv[4 * C], uu[4 * C];
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float gk = comp(avg[ch], k);
+                const float vk = a.beta2 * comp(sr.v[ch], k) + omb2 * (gk * gk);
+                const float mk = a.beta1 * comp(sr.m[ch], k) + omb1 * gk;
+                set_comp(sr.v[ch], k, vk);
+                set_comp(sr.m[ch], k, mk);
+                mm[4 * ch + k] = mk;
+                vv[4 * ch + k] = vk;
+            }
+        }
+        adam_step<4 * C>(mm, vv, a.lr, uu);
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) set_comp(avg[ch], k, uu[4 * ch + k]);
+        }
+    }
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
         const int64_t n = base + (int64_t)ch * kChunk + 4 * lane;
@@ -1145,24 +1231,11 @@ __device__ __forceinline__ void server_input(const StepArgs& a, const float4 (&a
             u[ch] = zero4();
             continue;
         }
-        float4 avg = make_float4(avg_of(acc[ch].x, fN, invN, pow2), avg_of(acc[ch].y, fN, invN, pow2),
-                                 avg_of(acc[ch].z, fN, invN, pow2), avg_of(acc[ch].w, fN, invN, pow2));
         if (placement_of<PL>(a) == AT_SERVER) {
-            float4 mv = sr.m[ch];
-            float4 vv = sr.v[ch];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const float gk = comp(avg, k);
-                const float vk = a.beta2 * comp(vv, k) + omb2 * (gk * gk);
-                const float mk = a.beta1 * comp(mv, k) + omb1 * gk;
-                set_comp(vv, k, vk);
-                set_comp(mv, k, mk);
-                set_comp(avg, k, vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f);
-            }
-            st4<VEC, FULL>(a.m, n, a.d, mv);
-            st4<VEC, FULL>(a.v, n, a.d, vv);
+            st4<VEC, FULL>(a.m, n, a.d, sr.m[ch]);
+            st4<VEC, FULL>(a.v, n, a.d, sr.v[ch]);
         }
-        u[ch] = avg;
+        u[ch] = avg[ch];
     }
 }
 

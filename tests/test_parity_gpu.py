@@ -263,6 +263,36 @@ def test_extreme_magnitudes(kind, placement):
     pair.check_tie_budget()
 
 
+@pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
+@pytest.mark.parametrize("eps", [0.0, 1.0], ids=["v0=0", "v0=1"])
+def test_adam_magnitude_sweep(placement, eps):
+    """Each 512-element tile takes gradients of one binary exponent, from
+    2^-75 up to 2^45 (and 2^-149 .. 2^-140 subnormals in the first tiles): the
+    Adam moments of successive tiles fall inside, outside and across the range
+    in which the kernels form the square root and the division from the
+    hardware estimates without operand scaling, so the results on either side
+    of each bound are checked bit for bit against the oracle's sqrtf and '/'.
+    With v0 = 1 the second moments stay near 1 while |m| crosses its lower
+    bound."""
+    d, N = 512 * 131, 4
+    q = STOCH(4, O.SCALE_L2, 512)
+    pair = Pair(d, N, q, q, placement, seed=9, eps=eps)
+    rng = np.random.default_rng(21)
+    expo = np.concatenate([np.arange(-149, -139), np.arange(-75, 46)]).astype(np.float64)
+    assert expo.size * 512 == d
+    scale = np.repeat(np.exp2(expo), 512)
+    for t in range(1, 4):
+        sgn = rng.choice(np.array([-1.0, 1.0]), size=(N, d))
+        g = (sgn * rng.uniform(1.0, 2.0, (N, d)) * scale).astype(np.float32)
+        g[:, 3 * 512 + 7] = 0.0     # a zero moment in a subnormal tile
+        pair.step(t, g)
+        for name in ("x", "e_w", "e_s") + (("m", "v") if placement == O.ADAM_AT_SERVER else ("m_w", "v_w")):
+            got = getattr(pair.rb, name).cpu().numpy()
+            assert same_values(got, getattr(pair.ost, name)), f"step {t}: {name} differs"
+        assert pair.stats.resyncs == 0
+    pair.check_tie_budget()
+
+
 @pytest.mark.parametrize("kind", ["stoch2_max", "ex1"])
 def test_subnormal_learning_rate(kind):
     """Adam at the workers with lr = 1e-40: every worker's update, hence the
