@@ -33,7 +33,8 @@ def _message_bytes(q, d):
     return codes + 4 * nb * per
 
 
-@pytest.mark.parametrize("key", ["bert", "gpt2m", "resnet50", "resnet18", "bert_topk", "bert_randk"])
+@pytest.mark.parametrize("key", ["bert", "gpt2m", "resnet50", "resnet18", "bert_topk", "bert_randk", "bert_topk2048",
+                                 "bert_randk2048"])
 @pytest.mark.parametrize("placement", [0, 1], ids=["server", "worker"])
 def test_algorithmic_bytes(key, placement):
     cfg, w = _cfg(key, placement)

@@ -85,7 +85,8 @@ class Sample:
 S, Wk = O.ADAM_AT_SERVER, O.ADAM_AT_WORKER
 FULL_CASES = [("bert", S, 100), ("bert", Wk, 100), ("resnet18", S, 50), ("resnet18", Wk, 50),
               ("resnet50", S, 50), ("resnet50", Wk, 50), ("gpt2m", S, 10), ("gpt2m", Wk, 10),
-              ("bert_topk", S, 20), ("bert_topk", Wk, 20), ("bert_randk", S, 20)]
+              ("bert_topk", S, 20), ("bert_topk", Wk, 20), ("bert_randk", S, 20), ("bert_topk2048", S, 20),
+              ("bert_randk2048", S, 20)]
 
 
 @pytest.mark.parametrize("key,placement,T", FULL_CASES,

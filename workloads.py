@@ -89,6 +89,11 @@ WORKLOADS = {
                           SPARSE(Q_TOPK, 16, 512), SPARSE(Q_TOPK, 16, 512), 20, 4, "student_t"),
     "bert_randk": Workload("bert_randk", "BERT-base-sized d=110000000 N=16, random-16 of 512", 110_000_000, 16,
                            SPARSE(Q_RANDK, 16, 512), SPARSE(Q_RANDK, 16, 512), 20, 4, "student_t"),
+    # the same density on 2048-element buckets (8-chunk tiles)
+    "bert_topk2048": Workload("bert_topk2048", "BERT-base-sized d=110000000 N=16, top-64 of 2048", 110_000_000, 16,
+                              SPARSE(Q_TOPK, 64, 2048), SPARSE(Q_TOPK, 64, 2048), 20, 4, "student_t"),
+    "bert_randk2048": Workload("bert_randk2048", "BERT-base-sized d=110000000 N=16, random-64 of 2048", 110_000_000,
+                               16, SPARSE(Q_RANDK, 64, 2048), SPARSE(Q_RANDK, 64, 2048), 20, 4, "student_t"),
 }
 
 # The paper's toy problem (Section V-A): 500x500, 10 workers, beta 0.9, theta 0.99.
