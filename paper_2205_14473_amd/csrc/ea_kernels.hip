@@ -223,6 +223,16 @@ int step_waves(const StepArgs& a, int C, int K, const Special* sp, const SymKern
     return split && G < C ? C : G;
 }
 
+// Rows whose byte length is not a multiple of 128 share a cache line between
+// adjacent tiles.  Whole-tile launches of one tile per block then deal runs
+// of this many adjacent tiles to each XCD (block_slot): ResNet-18-sized
+// round 0.2930 -> 0.2847 ms (runs of 8: 0.2880, 32: 0.2863).  With two
+// tiles per block the pair's shared line is inside the block already, and
+// runs measured slower (ResNet-50-sized 2.108 -> 2.155-2.187 ms).
+#ifndef EA_XCD_RUN
+#define EA_XCD_RUN 16
+#endif
+
 // Tiles per block of the whole-tile launch.
 int main_tiles_per_block(int C, const Special* sp, const SymKernel* sk, const HalfKernel* hk)
 {
@@ -340,6 +350,7 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
     b.tile1 = nfull;
     const int bufs = handoff_bufs(a.N, C, G, K, limit);
     b.one_buffer = bufs == 1 ? 1 : 0;
+    b.xcd_run = (a.d * 4) % 128 != 0 && K == 1 ? EA_XCD_RUN : 1;
     const dim3 grid((unsigned)(nfull / K)), block((unsigned)(G * kWave));
     const size_t lds = round_lds_bytes(a.N, C, G, K, bufs);
     if (sp) {
@@ -372,6 +383,7 @@ hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Speci
     b.tile1 = a.ntiles;
     const int bufs = handoff_bufs(a.N, C, G, 1, limit);
     b.one_buffer = bufs == 1 ? 1 : 0;
+    b.xcd_run = 1;
     const dim3 grid((unsigned)(a.ntiles - nfull)), block((unsigned)(G * kWave));
     const size_t lds = round_lds_bytes(a.N, C, G, 1, bufs);
     if (sp) {

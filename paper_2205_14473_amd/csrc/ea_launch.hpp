@@ -43,6 +43,7 @@ struct StepArgs {
     int32_t worker;           // split calls: worker index (Philox stream)
     int32_t apply;            // server_kernel: also update x
     int32_t one_buffer;       // fused round, more workers than waves: single-buffered handoff
+    int32_t xcd_run;          // fused round: blocks of a group of 8*xcd_run take tiles XCD-major (1: none)
     // Step index read on the device (null: `t`, `lr`, `beta2` above hold the
     // step's values); the schedule then gives lr and beta2 at that step.
     const uint32_t* t_dev;

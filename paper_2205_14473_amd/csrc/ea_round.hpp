@@ -1865,6 +1865,25 @@ inline int round_waves(int N, int C, int K, size_t lds_limit, int placement)
     return cached[dev];
 }
 
+// The block's place in the launch's run of tiles.  The hardware deals
+// consecutive blocks to the 8 XCDs in turn.  With xcd_run = R > 1, the
+// blocks of each whole group of 8R take the group's tiles XCD-major: the
+// R blocks an XCD receives there take R adjacent slots, so a cache line
+// that two adjacent tiles share (rows whose length is not a multiple of
+// 128 bytes) is fetched into one L2 instead of two, while the tiles in
+// flight across the GPU stay one contiguous window.
+__device__ __forceinline__ int64_t block_slot(const StepArgs& a)
+{
+    const int64_t b = blockIdx.x;
+    const int64_t R = a.xcd_run;
+    if (R <= 1) return b;
+    const int64_t grp = 8 * R;
+    const int64_t g = b / grp;
+    if ((g + 1) * grp > (int64_t)gridDim.x) return b;     // the last, partial group as dealt
+    const int64_t i = b - g * grp;
+    return g * grp + (i % 8) * R + i / 8;
+}
+
 // The fused round.  With a one-bucket Q_w the worker scales are read from
 // wscales (computed beforehand); with a one-bucket Q_s the block stops after
 // the server input, which it leaves in ubuf with per-tile partial norms.
@@ -1903,7 +1922,7 @@ __global__ __launch_bounds__(max_round_waves(C) * kWave,
     float4* xfer = smem + table_floats(G) / 4;
     constexpr int K = kernel_tiles(C, FULL, PL, half_kernel<QW, QS, PL>());
     __shared__ double red[SplitServe<QS, C>::value && K == 1 ? C * kWave : 1];
-    const int64_t first = a.tile0 + (int64_t)blockIdx.x * K;
+    const int64_t first = a.tile0 + block_slot(a) * K;
     const int64_t left = a.tile1 - first;
     round_tiles<C, K, VEC, FULL, QW, QS, PL>(a, first, left < K ? (int)left : K, lut_w, lut_s, xfer, G, red);
 }

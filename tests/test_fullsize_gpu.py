@@ -141,7 +141,8 @@ def test_full_size_sampled(key, placement, T):
 
 
 @pytest.mark.parametrize("key,placement", [("bert", None), ("gpt2m", None), ("resnet50", None), ("bert_topk", None),
-                                           ("bert", O.ADAM_AT_WORKER)])
+                                           ("bert", O.ADAM_AT_WORKER), ("resnet18", None),
+                                           ("resnet18", O.ADAM_AT_WORKER)])
 def test_full_size_split_calls_equal_fused(key, placement):
     """The four split calls at full size give, output for output, the same
     bits as ea_step: both sum the workers in ascending order and run the same
