@@ -265,11 +265,18 @@ __device__ __forceinline__ void wave_or_and(uint32_t vo, uint32_t va, uint32_t& 
 // values are listed in element order at positions counted the same way.
 // Elements past d get key 0 and the highest indices, so they rank below
 // every element of the vector and are never kept.
-template <int C, bool FULL, class QT>
-__device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C], int64_t base, int nch, int64_t d,
-                                              uint32_t k0, uint32_t k1, uint32_t step, uint32_t sid,
-                                              float* __restrict__ vals, WordSink& sink, float4 (&deq)[C])
+//
+// FLAGS (random-k on tiles of 4 or more chunks, whose keys do not depend on
+// p): only the code words are sent, and the lane's kept flags are returned,
+// bit 4j + k for its element in chunk j, slot k; sparse_values then writes
+// the values from p, which is not read here.
+template <int C, bool FULL, class QT, bool FLAGS = false>
+__device__ __forceinline__ uint32_t sparsify_tile(const QDev& q, const float4 (&p)[C], int64_t base, int nch,
+                                                  int64_t d, uint32_t k0, uint32_t k1, uint32_t step, uint32_t sid,
+                                                  float* __restrict__ vals, WordSink& sink, float4 (&deq)[C])
 {
+    static_assert(!FLAGS || (C >= 4 && QT::fixed && QT::kind(QDev{}) == Q_RANDK), "flags first: wide random-k only");
+    uint32_t kbits_out = 0u;
     const int lane = lane_id();
     const int cpb = QT::cpb(q);
     const bool topk = QT::kind(q) == Q_TOPK;
@@ -516,6 +523,17 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
                     }
                     eq_before += tot;
                 }
+                if constexpr (FLAGS) {
+                    uint32_t nib = (kept[0] ? 1u : 0u) | (kept[1] ? 2u : 0u) | (kept[2] ? 4u : 0u) |
+                                   (kept[3] ? 8u : 0u);
+                    // kept opaque, so the shift below is not folded into
+                    // selects of constants (a register per constant)
+                    asm volatile("" : "+v"(nib));
+                    kbits_out |= nib << (4 * j);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) sink.put(__builtin_amdgcn_ballot_w64(kept[k]));
+                    continue;
+                }
                 uint64_t km[4];
                 uint32_t below = 0, tot = 0;
 #pragma unroll
@@ -538,9 +556,71 @@ __device__ __forceinline__ void sparsify_tile(const QDev& q, const float4 (&p)[C
             }
         }
         // A bucket shorter than keep: the remaining value slots are zero.
+        if (!FULL && !FLAGS)
+            for (uint32_t sl = kk + (uint32_t)lane; sl < (uint32_t)q.keep; sl += kWave) vb[sl] = 0.0f;
+    }
+    return kbits_out;
+}
+
+// The values of a sparsified tile whose kept flags are known (bit 4j + k of
+// a lane for its element in chunk j, slot k, from sparsify_tile<..., true>,
+// which has sent the code words): per bucket the kept values in element
+// order, zeros in the value slots past a short bucket's kk, and the
+// dequantized tile.
+template <int C, bool FULL, class QT>
+__device__ __forceinline__ void sparse_values(const QDev& q, const float4 (&p)[C], uint32_t kbits, int64_t base,
+                                              int nch, int64_t d, float* __restrict__ vals, float4 (&deq)[C])
+{
+    const int lane = lane_id();
+    const int cpb = QT::cpb(q);
+    if (FULL) nch = C;
+    const int64_t chunk0 = base >> 8;
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch) deq[ch] = zero4();
+#pragma unroll
+    for (int b0 = 0; b0 < C; ++b0) {
+        if ((b0 & (cpb - 1)) != 0) continue;
+        if (!FULL && b0 >= nch) continue;
+        const int64_t e0 = base + (int64_t)b0 * kChunk;
+        const int64_t nb = FULL ? q.B : ((d - e0) < q.B ? (d - e0) : q.B);
+        const uint32_t kk = (uint32_t)(nb < q.keep ? nb : q.keep);
+        float* vb = vals + ((chunk0 + b0) >> QT::cpb_shift(q)) * (int64_t)q.keep;
+        uint32_t kept_before = 0;
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+            if (j < b0 || j >= b0 + cpb) continue;
+            if (!FULL && j >= nch) continue;
+            uint32_t below = 0, tot = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint64_t km = __builtin_amdgcn_ballot_w64(((kbits >> (4 * j + k)) & 1u) != 0u);
+                below += lanes_below(km);
+                tot += (uint32_t)__builtin_popcountll(km);
+            }
+            uint32_t own = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const bool kept = ((kbits >> (4 * j + k)) & 1u) != 0u;
+                const float x = comp(p[j], k);
+                const uint32_t pos = kept_before + below + own;   // < kk by construction; guarded all the same
+                if (kept && pos < (uint32_t)q.keep) vb[pos] = x;
+                own += kept ? 1u : 0u;
+                set_comp(deq[j], k, kept ? x : 0.0f);
+            }
+            kept_before += tot;
+        }
         if (!FULL)
             for (uint32_t sl = kk + (uint32_t)lane; sl < (uint32_t)q.keep; sl += kWave) vb[sl] = 0.0f;
     }
+}
+
+// Sparsifiers whose selection runs before the values exist: random-k on
+// tiles of 4 or more chunks (its keys are draws).  The draws and the
+// selection then do not hold registers beside the tile's values.
+template <class QT, int C>
+__host__ __device__ constexpr bool select_first()
+{
+    return C >= 4 && QT::fixed && QT::kind(QDev{}) == Q_RANDK;
 }
 
 template <int C, bool FULL, class QT>
@@ -1290,11 +1370,24 @@ __device__ __forceinline__ void worker_compute(const StepArgs& a, const TilePos&
     const bool atw = placement_of<PL>(a) == AT_WORKER;
     const int64_t row = (int64_t)i * a.d;
     float4 p[C], dq[C];
-    worker_p<C, PL>(a, r, p);
-    if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
-    const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
-    quantize_tile<C, FULL, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
-                               a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales, sink, dq);
+    if constexpr (select_first<QW, C>()) {
+        // the selection and the code words first, while the rows arrive
+        float4 none[C];
+#pragma unroll
+        for (int ch = 0; ch < C; ++ch) none[ch] = zero4();
+        const uint32_t kb = sparsify_tile<C, FULL, QW, true>(a.qw, none, t.base, t.nch, a.d, a.k0, a.k1, a.t,
+                                                             (uint32_t)i, nullptr, sink, dq);
+        worker_p<C, PL>(a, r, p);
+        if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
+        sparse_values<C, FULL, QW>(a.qw, p, kb, t.base, t.nch, a.d, a.wscales + (int64_t)i * a.qw.nscales, dq);
+    } else {
+        worker_p<C, PL>(a, r, p);
+        if (atw) store_moments<C, VEC, FULL, PL>(a, a.m_w + row, a.v_w + row, t.base, t.nch, r);
+        const float gs = wglobal ? a.wscales[(int64_t)i * a.qw.nscales] : 0.0f;
+        quantize_tile<C, FULL, QW>(a.qw, lut_w, p, t.base, t.nch, a.d, a.k0, a.k1, a.t, (uint32_t)i, gs,
+                                   a.wcodes + (int64_t)i * a.qw.words, a.wscales + (int64_t)i * a.qw.nscales, sink,
+                                   dq);
+    }
     float* e = a.e_w + row;
 #pragma unroll
     for (int ch = 0; ch < C; ++ch) {
@@ -1517,11 +1610,21 @@ __device__ __forceinline__ void serve_sparse(const StepArgs& a, const TilePos& t
     __syncthreads();                           // q and x of every chunk are in LDS
     if (w != 0) return;
     float4 q[C], dq[C];
-#pragma unroll
-    for (int j = 0; j < C; ++j) q[j] = (FULL || j < nch) ? slots[j * kWave + lane] : zero4();
     WordSink sink = message_sink<QS>(a.qs, a.scodes, t.base);
-    quantize_tile<C, FULL, QS>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, 0.0f, a.scodes,
-                               a.sscales, sink, dq);
+    if constexpr (select_first<QS, C>()) {
+#pragma unroll
+        for (int j = 0; j < C; ++j) q[j] = zero4();
+        const uint32_t kb = sparsify_tile<C, FULL, QS, true>(a.qs, q, t.base, t.nch, a.d, a.k0, a.k1, a.t,
+                                                             kServerStream, nullptr, sink, dq);
+#pragma unroll
+        for (int j = 0; j < C; ++j) q[j] = (FULL || j < nch) ? slots[j * kWave + lane] : zero4();
+        sparse_values<C, FULL, QS>(a.qs, q, kb, t.base, t.nch, a.d, a.sscales, dq);
+    } else {
+#pragma unroll
+        for (int j = 0; j < C; ++j) q[j] = (FULL || j < nch) ? slots[j * kWave + lane] : zero4();
+        quantize_tile<C, FULL, QS>(a.qs, lut_s, q, t.base, t.nch, a.d, a.k0, a.k1, a.t, kServerStream, 0.0f,
+                                   a.scodes, a.sscales, sink, dq);
+    }
     sink.flush();
 #pragma unroll
     for (int j = 0; j < C; ++j) {
