@@ -264,6 +264,16 @@ def test_extreme_magnitudes(kind, placement):
 
 
 @pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
+def test_xcd_runs_cover_every_tile(placement):
+    """Rows whose byte length is not a multiple of 128 (d = 8 mod 32), one
+    2048-element tile per block: the whole-tile launch deals each whole group
+    of 128 blocks XCD-major.  300 whole tiles make two whole groups and a
+    partial one, plus the ragged tile; every element is checked."""
+    d, N = 2048 * 300 + 8, 8
+    _run(d, N, SIGN(2048), SIGN(2048), placement, T=2, gen="segscale", seed=13)
+
+
+@pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
 @pytest.mark.parametrize("eps", [0.0, 1.0], ids=["v0=0", "v0=1"])
 def test_adam_magnitude_sweep(placement, eps):
     """Each 512-element tile takes gradients of one binary exponent, from
