@@ -266,8 +266,8 @@ __device__ __forceinline__ void wave_or_and(uint32_t vo, uint32_t va, uint32_t& 
 // Elements past d get key 0 and the highest indices, so they rank below
 // every element of the vector and are never kept.
 //
-// FLAGS (random-k on tiles of 4 or more chunks, whose keys do not depend on
-// p): only the code words are sent, and the lane's kept flags are returned,
+// FLAGS (random-k on wide tiles, whose keys do not depend on p): only the
+// code words are sent, and the lane's kept flags are returned,
 // bit 4j + k for its element in chunk j, slot k; sparse_values then writes
 // the values from p, which is not read here.
 template <int C, bool FULL, class QT, bool FLAGS = false>
@@ -615,12 +615,17 @@ __device__ __forceinline__ void sparse_values(const QDev& q, const float4 (&p)[C
 }
 
 // Sparsifiers whose selection runs before the values exist: random-k on
-// tiles of 4 or more chunks (its keys are draws).  The draws and the
-// selection then do not hold registers beside the tile's values.
+// 8-chunk tiles (its keys are draws).  The draws and the selection then do
+// not hold registers beside the tile's values (random-64 of 2048 5.7 -> 5.0
+// ms); on 4-chunk tiles, which have registers to spare, it measured slower
+// (random-32 of 1024 4.7 -> 5.0 ms).
+#ifndef EA_SELECT_FIRST_MIN_C
+#define EA_SELECT_FIRST_MIN_C 8
+#endif
 template <class QT, int C>
 __host__ __device__ constexpr bool select_first()
 {
-    return C >= 4 && QT::fixed && QT::kind(QDev{}) == Q_RANDK;
+    return C >= EA_SELECT_FIRST_MIN_C && QT::fixed && QT::kind(QDev{}) == Q_RANDK;
 }
 
 template <int C, bool FULL, class QT>
