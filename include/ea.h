@@ -23,6 +23,13 @@
  *     Arguments are validated before any device work is enqueued, so an
  *     invalid call enqueues nothing and touches no device state.
  *   - Vectors are IEEE binary32.  Per-worker arrays are row-major [N][d].
+ *   - Device pointers must be 4-byte aligned (else EA_ERR_ALIGN).  The whole-
+ *     tile kernels need 16-byte aligned rows: every binary32 vector of the
+ *     call 16-byte aligned (and an EA_Q_NONE message buffer) and d a multiple
+ *     of 4, so that each row of an [N][d] array starts 16-byte aligned.  Any
+ *     other accepted layout runs on kernels with per-element bounds checks,
+ *     with the same results, about twice as slow.  Rows whose byte length is
+ *     a multiple of 128 also share no cache line between tiles.
  *   - Calls that share buffers must be ordered by the caller (same stream).
  *
  * Wire format of a message (the paper defines none)
