@@ -85,6 +85,30 @@ def test_wide_tile_kernels(kind, d, N, keep):
     _run(d, N, q, q, O.ADAM_AT_SERVER, T=3, seed=keep)
 
 
+def _random_wide_cases(n, seed=77):
+    rng = np.random.default_rng(seed)
+    out = []
+    for j in range(n):
+        kind = ("topk", "randk")[j % 2]
+        placement = (O.ADAM_AT_SERVER, O.ADAM_AT_WORKER)[(j // 2) % 2]
+        d = int(rng.integers(1, 12)) * 2048 + int(rng.integers(0, 2048))
+        N = int(rng.integers(1, 41))
+        keep = int(rng.choice([1, int(rng.integers(2, 129)), int(rng.integers(129, 2049))]))
+        out.append((kind, placement, d, N, keep))
+    return out
+
+
+@pytest.mark.parametrize("kind,placement,d,N,keep", _random_wide_cases(12))
+def test_wide_tile_random_shapes(kind, placement, d, N, keep):
+    """Seeded random shapes on 2048-element buckets: d up to 12 tiles with a
+    ragged tail, 1 to 40 workers (up to five worker groups of eight waves),
+    keep from 1 to 2048, both placements (the fully specialized kernels with
+    Adam at the server, the worker-specialized ones with Adam at the
+    workers; random-k selects before reading the values on both)."""
+    q = SPARSE[kind](keep, 2048)
+    _run(d, N, q, q, placement, T=2, seed=N + keep)
+
+
 @pytest.mark.parametrize("kind", list(SPARSE))
 def test_split_calls(kind):
     q = SPARSE[kind](24, 512)
