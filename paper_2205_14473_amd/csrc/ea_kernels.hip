@@ -209,13 +209,16 @@ hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Speci
                             size_t limit, hipStream_t s);
 
 // Waves per block of a fused-round launch: one per worker up to the tile's
-// limit.  Fully specialized 8-chunk tiles serve a whole-tile server bucket,
-// or a sparsifier's server side, on C waves, one chunk each (SplitServe,
+// limit, and at least one per tile of the block, since wave k serves tile k
+// (with fewer workers than tiles the other waves only serve).  Fully
+// specialized 8-chunk tiles serve a whole-tile server bucket, or a
+// sparsifier's server side, on C waves, one chunk each (SplitServe,
 // SparseServe; whole and ragged tiles alike), so their blocks have C waves
 // at least.
 int step_waves(const StepArgs& a, int C, int K, const Special* sp, const SymKernel* sk, size_t limit)
 {
-    const int G = round_waves(a.N, C, K, limit, a.placement);
+    int G = round_waves(a.N, C, K, limit, a.placement);
+    if (G < K) G = K;
     const bool scaled = a.qs.cpb == C &&
                         (a.qs.kind == Q_SCALED_SIGN || a.qs.kind == Q_STOCH || a.qs.kind == Q_DET);
     const bool sparse = a.qs.kind == Q_TOPK || a.qs.kind == Q_RANDK;
@@ -338,6 +341,14 @@ hipError_t launch_step(const StepArgs& a, int C, bool vec, hipStream_t s, bool s
 
 namespace {
 
+// One dispatch covers at most 2^32 - 1 work-items, and the fused kernels run
+// up to four threads per element (one-chunk tiles, 16 waves, one tile per
+// block), so a whole-tile launch is issued in pieces of at most this many
+// blocks (2^30 threads): one piece up to d = 2^28 in that shape, 2^30 in
+// the BERT-sized one.  Pieces are multiples of 128 blocks, so the XCD runs
+// of block_slot keep their groups.
+constexpr int64_t kMaxLaunchBlocks = (int64_t)1 << 20;
+
 // The whole tiles [0, nfull) of a round, nfull a multiple of the kernel's
 // tiles per block (launch_step).
 hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Special* sp, const SymKernel* sk,
@@ -346,29 +357,36 @@ hipError_t launch_step_main(const StepArgs& a, int C, int64_t nfull, const Speci
     const int K = main_tiles_per_block(C, sp, sk, hk);
     const int G = step_waves(a, C, K, sp, sk, limit);
     StepArgs b = a;
-    b.tile0 = 0;
-    b.tile1 = nfull;
     const int bufs = handoff_bufs(a.N, C, G, K, limit);
     b.one_buffer = bufs == 1 ? 1 : 0;
     b.xcd_run = (a.d * 4) % 128 != 0 && K == 1 ? EA_XCD_RUN : 1;
-    const dim3 grid((unsigned)(nfull / K)), block((unsigned)(G * kWave));
+    const dim3 block((unsigned)(G * kWave));
     const size_t lds = round_lds_bytes(a.N, C, G, K, bufs);
-    if (sp) {
-        hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
-    } else if (sk) {
-        hipLaunchKernelGGL(sk->kernel, grid, block, lds, s, b);
-    } else if (hk) {
-        hipLaunchKernelGGL(hk->kernel, grid, block, lds, s, b);
-    } else {
-        switch (C) {
-        case 1: hipLaunchKernelGGL((step_kernel<1, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-        case 2: hipLaunchKernelGGL((step_kernel<2, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-        case 4: hipLaunchKernelGGL((step_kernel<4, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-        case 8: hipLaunchKernelGGL((step_kernel<8, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
-        default: return hipErrorInvalidValue;
+    const int64_t nblocks = nfull / K;
+    for (int64_t b0 = 0; b0 < nblocks; b0 += kMaxLaunchBlocks) {
+        const int64_t nb = nblocks - b0 < kMaxLaunchBlocks ? nblocks - b0 : kMaxLaunchBlocks;
+        b.tile0 = b0 * K;
+        b.tile1 = (b0 + nb) * K;
+        const dim3 grid((unsigned)nb);
+        if (sp) {
+            hipLaunchKernelGGL(sp->kernel, grid, block, lds, s, b);
+        } else if (sk) {
+            hipLaunchKernelGGL(sk->kernel, grid, block, lds, s, b);
+        } else if (hk) {
+            hipLaunchKernelGGL(hk->kernel, grid, block, lds, s, b);
+        } else {
+            switch (C) {
+            case 1: hipLaunchKernelGGL((step_kernel<1, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 2: hipLaunchKernelGGL((step_kernel<2, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 4: hipLaunchKernelGGL((step_kernel<4, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 8: hipLaunchKernelGGL((step_kernel<8, true, true, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            default: return hipErrorInvalidValue;
+            }
         }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 // The tiles [nfull, ntiles) of a round (at most one short of a whole-tile
@@ -379,29 +397,34 @@ hipError_t launch_step_edge(const StepArgs& a, int C, int64_t nfull, const Speci
 {
     const int G = step_waves(a, C, 1, sp, sk, limit);
     StepArgs b = a;
-    b.tile0 = nfull;
-    b.tile1 = a.ntiles;
     const int bufs = handoff_bufs(a.N, C, G, 1, limit);
     b.one_buffer = bufs == 1 ? 1 : 0;
     b.xcd_run = 1;
-    const dim3 grid((unsigned)(a.ntiles - nfull)), block((unsigned)(G * kWave));
+    const dim3 block((unsigned)(G * kWave));
     const size_t lds = round_lds_bytes(a.N, C, G, 1, bufs);
-    if (sp) {
-        hipLaunchKernelGGL(sp->edge, grid, block, lds, s, b);
-        return hipGetLastError();
+    // one tile per block; every tile of a round with unaligned rows comes
+    // here, so the launch is issued in pieces as the whole-tile one is
+    for (int64_t t0 = nfull; t0 < a.ntiles; t0 += kMaxLaunchBlocks) {
+        b.tile0 = t0;
+        b.tile1 = a.ntiles - t0 < kMaxLaunchBlocks ? a.ntiles : t0 + kMaxLaunchBlocks;
+        const dim3 grid((unsigned)(b.tile1 - b.tile0));
+        if (sp) {
+            hipLaunchKernelGGL(sp->edge, grid, block, lds, s, b);
+        } else if (sk) {
+            hipLaunchKernelGGL(sk->edge, grid, block, lds, s, b);
+        } else {
+            switch (C) {
+            case 1: hipLaunchKernelGGL((step_kernel<1, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 2: hipLaunchKernelGGL((step_kernel<2, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 4: hipLaunchKernelGGL((step_kernel<4, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            case 8: hipLaunchKernelGGL((step_kernel<8, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
+            default: return hipErrorInvalidValue;
+            }
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    if (sk) {
-        hipLaunchKernelGGL(sk->edge, grid, block, lds, s, b);
-        return hipGetLastError();
-    }
-    switch (C) {
-    case 1: hipLaunchKernelGGL((step_kernel<1, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
-    case 2: hipLaunchKernelGGL((step_kernel<2, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
-    case 4: hipLaunchKernelGGL((step_kernel<4, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
-    case 8: hipLaunchKernelGGL((step_kernel<8, false, false, QRt, QRt, -1>), grid, block, lds, s, b); break;
-    default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace

@@ -95,8 +95,33 @@ def test_full_size_sampled(key, placement, T):
     """Each workload at its real d and N through ea_step, both placements,
     for its step count (100 for the BERT-sized round): after every step the
     sampled segments' messages and state equal the oracle's bit for bit."""
-    w = W.WORKLOADS[key]
+    _sampled_rounds(W.WORKLOADS[key], placement, T)
+
+
+@pytest.mark.parametrize("placement", [S, Wk], ids=["server", "worker"])
+@pytest.mark.parametrize("tail", [76, 77], ids=["aligned", "unaligned"])
+def test_launch_in_pieces(placement, tail):
+    """Launches of more than 2^20 blocks are issued in pieces.  Scaled sign on
+    256-element buckets with one worker: with d = 2^29 + 512 + 76 (rows
+    16-byte aligned) the whole-tile kernel takes two tiles per block, 2^20 + 1
+    blocks (two pieces), and the checked one the ragged tile; with d = 2^29 +
+    512 + 77 (unaligned rows) the checked kernel takes every tile, one per
+    block (three pieces).  The segments on both sides of the piece boundaries
+    at elements 2^28 and 2^29, the first and the last are checked against the
+    oracle after every step."""
+    sign = W.SIGN1(256)
+    d = (1 << 29) + 2 * 256 + tail
+    w = W.Workload("pieces", f"d=2^29+{512 + tail} N=1, sign 256", d, 1, sign, sign, 2, 31, "student_t")
+    tile = 512
+    ntiles = -(-d // tile)
+    b = (1 << 29) // tile        # the first segment of the second piece
+    picks = sorted({0, 1, b // 2 - 1, b // 2, b - 2, b - 1, b, b + 1, ntiles - 1})
+    _sampled_rounds(w, placement, 2, [(k * tile, min(tile, d - k * tile)) for k in picks])
+
+
+def _sampled_rounds(w, placement, T, segs=None):
     d, N = w.d, w.N
+    key = w.key
     print(f"\n[fullsize] {w.name} placement={placement} T={T}", flush=True)
     oc, ec = configs(d, N, w.qw.fields(), w.qs.fields(), placement, w.seed, w.beta1, w.beta2, w.lr, w.eps)
     rb = allocate(ec)
@@ -106,7 +131,7 @@ def test_full_size_sampled(key, placement, T):
     torch.randn(d, generator=gen, device="cuda", out=rb.x)
     rb.x.mul_(0.02)
     tile = max(O.bucket_len(oc.qw, d), O.bucket_len(oc.qs, d), 512)
-    smp = Sample(oc, d, _segments(d, tile, 24, w.seed))
+    smp = Sample(oc, d, segs if segs is not None else _segments(d, tile, 24, w.seed))
     x_host = smp.vec(rb.x)
     states = [O.State.init(oc, ln, x_host[a["e"]]) for (n0, ln), a in zip(smp.segs, smp.at)]
     stats = Stats()

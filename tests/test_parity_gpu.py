@@ -263,6 +263,23 @@ def test_extreme_magnitudes(kind, placement):
     pair.check_tie_budget()
 
 
+ONE_WORKER = [
+    ("stoch4_512", STOCH(4, O.SCALE_L2, 512), O.ADAM_AT_SERVER, 512 * 9 + 300),
+    ("topk16_512", qfields(O.Q_TOPK, bucket=512, keep=16), O.ADAM_AT_SERVER, 512 * 12 + 64),
+    ("sign_256_server", SIGN(256), O.ADAM_AT_SERVER, 256 * 13 + 52),
+    ("sign_256_worker", SIGN(256), O.ADAM_AT_WORKER, 256 * 13 + 52),
+    ("stoch2_256", STOCH(2, O.SCALE_MAX, 256), O.ADAM_AT_SERVER, 256 * 6),
+]
+
+
+@pytest.mark.parametrize("name,q,placement,d", ONE_WORKER, ids=[c[0] for c in ONE_WORKER])
+def test_one_worker_two_tile_blocks(name, q, placement, d):
+    """One worker on kernels that take two tiles per block (the specialized
+    512-element kernels, the worker-specialized 256-element ones): the block
+    still has a wave for each tile's server side."""
+    _run(d, 1, q, q, placement, T=3, seed=17)
+
+
 @pytest.mark.parametrize("placement", [O.ADAM_AT_SERVER, O.ADAM_AT_WORKER], ids=["server", "worker"])
 def test_xcd_runs_cover_every_tile(placement):
     """Rows whose byte length is not a multiple of 128 (d = 8 mod 32), one
