@@ -76,3 +76,44 @@ def test_random_config(d, N, qw, qs, placement, split, gen, seed):
         pair.step(t, W.host_gradients(w, t, d=d))
     pair.check_tie_budget()
     assert pair.stats.resyncs == 0
+
+
+# The quantizer pairs of the fully specialized kernels (the benchmark shapes).
+SPECIAL_PAIRS = [
+    ("stoch4l2_512", qfields(O.Q_STOCH_UNIFORM, 4, O.SCALE_L2, 1, 512), qfields(O.Q_STOCH_UNIFORM, 4, O.SCALE_L2, 1, 512)),
+    ("stoch2max_512", qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, 1, 512),
+     qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, 1, 512)),
+    ("stoch2max_1024/sign1024", qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, 1, 1024),
+     qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 1, 1024)),
+    ("sign2048", qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 1, 2048), qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 1, 2048)),
+    ("topk16_512", qfields(O.Q_TOPK, bucket=512, keep=16), qfields(O.Q_TOPK, bucket=512, keep=16)),
+    ("randk16_512", qfields(O.Q_RANDK, bucket=512, keep=16), qfields(O.Q_RANDK, bucket=512, keep=16)),
+    ("topk64_2048", qfields(O.Q_TOPK, bucket=2048, keep=64), qfields(O.Q_TOPK, bucket=2048, keep=64)),
+    ("randk64_2048", qfields(O.Q_RANDK, bucket=2048, keep=64), qfields(O.Q_RANDK, bucket=2048, keep=64)),
+]
+
+
+def _special_cases(n, seed=2025):
+    rng = np.random.default_rng(seed)
+    out = []
+    for j in range(n):
+        name, qw, qs = SPECIAL_PAIRS[j % len(SPECIAL_PAIRS)]
+        d = 2048 * int(rng.integers(1, 40)) + int(rng.integers(0, 2048)) // 4 * 4 + (0 if rng.random() < 0.8 else 1)
+        N = int(rng.choice([1, 2, 3, int(rng.integers(4, 17)), int(rng.integers(17, 41))]))
+        placement = int(rng.choice([O.ADAM_AT_SERVER, O.ADAM_AT_WORKER]))
+        out.append(pytest.param(d, N, qw, qs, placement, 300 + j,
+                                id=f"{j}-{name}-d{d}-N{N}-{'srv' if placement == 0 else 'wrk'}"))
+    return out
+
+
+@pytest.mark.parametrize("d,N,qw,qs,placement,seed", _special_cases(32))
+def test_random_specialized_shapes(d, N, qw, qs, placement, seed):
+    """The benchmark shapes' quantizer pairs (fully specialized kernels) with
+    random worker counts (1 to 40: one wave per tile or per worker, several
+    worker groups) and sizes (aligned or not, with ragged tails)."""
+    pair = Pair(d, N, qw, qs, placement, seed=seed)
+    for t in range(1, 3):
+        w = W.Workload("r", "r", d, N, None, None, 1, seed, "student_t")
+        pair.step(t, W.host_gradients(w, t, d=d))
+    pair.check_tie_budget()
+    assert pair.stats.resyncs == 0
