@@ -117,3 +117,39 @@ def test_random_specialized_shapes(d, N, qw, qs, placement, seed):
         pair.step(t, W.host_gradients(w, t, d=d))
     pair.check_tie_budget()
     assert pair.stats.resyncs == 0
+
+
+SCHEDULES = [
+    dict(kind=O.SCHED_CONSTANT),
+    dict(kind=O.SCHED_ASSUMPTION2, alpha=2e-3, theta=0.99, T=400),
+    dict(kind=O.SCHED_STEP_DECAY, alpha=1e-3, factor=0.5, period=1),
+]
+
+
+def _scheduled_cases(n, seed=2026):
+    rng = np.random.default_rng(seed)
+    out = []
+    for j in range(n):
+        d = (int(rng.integers(1, 700)) if j % 3 == 0 else 512 * int(rng.integers(1, 30)) + int(rng.integers(0, 512)))
+        N = int(rng.integers(1, 21))
+        nw, qw = _quant(rng)
+        ns, qs = _quant(rng)
+        placement = int(rng.choice([O.ADAM_AT_SERVER, O.ADAM_AT_WORKER]))
+        sched = int(rng.integers(0, len(SCHEDULES)))
+        mode = ("scheduled", "run")[j % 2]
+        out.append(pytest.param(d, N, qw, qs, placement, sched, mode, 500 + j,
+                                id=f"{j}-d{d}-N{N}-{nw}-{ns}-{'srv' if placement == 0 else 'wrk'}-s{sched}-{mode}"))
+    return out
+
+
+@pytest.mark.parametrize("d,N,qw,qs,placement,sched,mode,seed", _scheduled_cases(16))
+def test_random_scheduled_rounds(d, N, qw, qs, placement, sched, mode, seed):
+    """Random configurations through ea_step_scheduled (the step read on the
+    device, lr_t and beta2_t from the schedule in the kernels) and ea_run,
+    three steps each, against the oracle's own schedule."""
+    pair = Pair(d, N, qw, qs, placement, seed=seed, sched=SCHEDULES[sched], mode=mode)
+    for t in range(1, 4):
+        w = W.Workload("r", "r", d, N, None, None, 1, seed, "student_t")
+        pair.step(t, W.host_gradients(w, t, d=d))
+    pair.check_tie_budget()
+    assert pair.stats.resyncs == 0
