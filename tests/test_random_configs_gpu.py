@@ -126,7 +126,7 @@ SCHEDULES = [
 ]
 
 
-def _scheduled_cases(n, seed=2026):
+def _scheduled_cases(n, seed=2026, modes=("scheduled", "run")):
     rng = np.random.default_rng(seed)
     out = []
     for j in range(n):
@@ -136,17 +136,20 @@ def _scheduled_cases(n, seed=2026):
         ns, qs = _quant(rng)
         placement = int(rng.choice([O.ADAM_AT_SERVER, O.ADAM_AT_WORKER]))
         sched = int(rng.integers(0, len(SCHEDULES)))
-        mode = ("scheduled", "run")[j % 2]
+        mode = modes[j % len(modes)]
         out.append(pytest.param(d, N, qw, qs, placement, sched, mode, 500 + j,
                                 id=f"{j}-d{d}-N{N}-{nw}-{ns}-{'srv' if placement == 0 else 'wrk'}-s{sched}-{mode}"))
     return out
 
 
-@pytest.mark.parametrize("d,N,qw,qs,placement,sched,mode,seed", _scheduled_cases(16))
+@pytest.mark.parametrize("d,N,qw,qs,placement,sched,mode,seed",
+                         _scheduled_cases(16) + _scheduled_cases(8, seed=2027, modes=("graph",)))
 def test_random_scheduled_rounds(d, N, qw, qs, placement, sched, mode, seed):
     """Random configurations through ea_step_scheduled (the step read on the
-    device, lr_t and beta2_t from the schedule in the kernels) and ea_run,
-    three steps each, against the oracle's own schedule."""
+    device, lr_t and beta2_t from the schedule in the kernels), ea_run, and a
+    HIP graph of ea_step_scheduled captured once and replayed every step
+    (eager copies and synchronizations between the replays), three steps
+    each, against the oracle's own schedule."""
     pair = Pair(d, N, qw, qs, placement, seed=seed, sched=SCHEDULES[sched], mode=mode)
     for t in range(1, 4):
         w = W.Workload("r", "r", d, N, None, None, 1, seed, "student_t")
