@@ -83,3 +83,30 @@ def test_noalloc_rejects_configurations_beyond_its_scratch():
         E.ea_step_noalloc(ec, 1, *([1 << 20] * 12))
     assert ei.value.code == E.EA_ERR_UNSUPPORTED
     assert "scratch" in E.ea_last_error()
+
+
+ONE_BUCKET_OR_NOT = [
+    SIGN0, STOCH2MAX0, EX1_0, STOCH4,
+    qfields(O.Q_STOCH_UNIFORM, 8, O.SCALE_L2, 1, 0),
+    qfields(O.Q_SCALED_SIGN, 1, O.SCALE_L1, 0, 0),
+    qfields(O.Q_TOPK, bucket=1024, keep=40),
+    qfields(O.Q_POW2, kmin=-30, kmax=-2),
+]
+
+
+@pytest.mark.parametrize("j", range(10))
+def test_noalloc_random_configurations(j):
+    """Seeded random configurations (one-bucket and bucketed quantizers, 1 to
+    12 workers, either placement), three rounds through ea_step_noalloc after
+    the calls above left other contents in the scratch array: bit-identical to
+    ea_step with a workspace of the caller's."""
+    rng = np.random.default_rng(700 + j)
+    d = int(rng.integers(1, 300_000))
+    N = int(rng.integers(1, 13))
+    qw = ONE_BUCKET_OR_NOT[int(rng.integers(0, len(ONE_BUCKET_OR_NOT)))]
+    qs = ONE_BUCKET_OR_NOT[int(rng.integers(0, len(ONE_BUCKET_OR_NOT)))]
+    placement = int(rng.choice([O.ADAM_AT_SERVER, O.ADAM_AT_WORKER]))
+    ec, a, b, w = _pair(d, N, qw, qs, placement, 700 + j)
+    assert E.ea_workspace_bytes(ec) <= E.EA_NOALLOC_SCRATCH_BYTES
+    for t in range(1, 4):
+        _round(ec, a, b, w, t, d)
