@@ -67,8 +67,7 @@
  *                 words.
  *
  * Buckets: `bucket` is 0 (one bucket over the whole vector), >= d (same), or
- * a multiple of 256 up to 2048; when both sides are bucketed, the larger of
- * the two buckets must be a multiple of the smaller.  TOPK and RANDK need
+ * 256, 512, 1024 or 2048 (other sizes return EA_ERR_UNSUPPORTED).  TOPK and RANDK need
  * bucket 256, 512, 1024 or 2048 (a bucket >= d is one short bucket) and
  * 1 <= keep <= bucket.
  *

@@ -239,3 +239,47 @@ def test_toy_step_rejects_scaled_quantizers_before_device_work(E):
     with pytest.raises(E.EAError) as ei:
         E.ea_toy_step(c2, 1, *([1 << 20] * 15), stream=0)
     assert ei.value.code == E.EA_ERR_ARG
+
+
+def test_random_quantizer_fields(E):
+    """2,000 seeded random quantizer records, valid and invalid: validation
+    never fails without a message, accepts exactly the records the header's
+    rules allow, and every accepted record's message sizes agree with the
+    oracle's at random d."""
+    import numpy as np
+    rng = np.random.default_rng(99)
+    ok_count = 0
+    for _ in range(2000):
+        qd = dict(kind=int(rng.integers(-1, 8)), scale=int(rng.integers(-1, 4)), bits=int(rng.integers(-1, 34)),
+                  error_feedback=int(rng.integers(-1, 3)), bucket=int(rng.choice([-256, 0, 128, 256, 512, 768, 1024,
+                                                                                  2048, 4096, 1 << 20])),
+                  pow2_kmin=int(rng.integers(-130, 10)), pow2_kmax=int(rng.integers(-130, 130)),
+                  keep=int(rng.integers(-1, 2100)))
+        d = int(rng.integers(1, 1 << 21))
+        cfg = _cfg(E, d=d, qw=E.Quant(**qd))
+        rc = E.ea_validate(cfg)
+        if rc != 0:
+            assert rc in (-1, -4), (qd, rc)
+            assert E.ea_last_error() != ""
+            continue
+        ok_count += 1
+        k, b, B = qd["kind"], qd["bits"], qd["bucket"]
+        # what the header allows (a bucket >= d is one bucket)
+        assert k in (0, 1, 2, 3, 4, 5, 6), qd
+        assert qd["error_feedback"] in (0, 1), qd
+        if k == 2:
+            assert b in (1, 2, 4, 8) and qd["scale"] in (1, 2), qd
+        if k == 3:
+            assert 2 <= b <= 8, qd
+        if k == 4:
+            assert -126 <= qd["pow2_kmin"] < qd["pow2_kmax"] <= 127, qd
+        if k in (1, 2, 3):
+            assert B in (0, 256, 512, 1024, 2048) or B >= d, qd
+        if k in (5, 6):
+            assert (B in (256, 512, 1024, 2048) or B >= d) and 1 <= qd["keep"] <= min(B, max(B, d)), qd
+        qo = O.Quant(**qd)
+        qe = E.Quant(**qd)
+        assert E.ea_code_bits(qe) == O.code_bits(qo), qd
+        assert E.ea_msg_words(qe, d) == O.msg_words(qo, d), (qd, d)
+        assert E.ea_msg_scales(qe, d) == O.num_scales(qo, d, d), (qd, d)
+    assert ok_count > 100
