@@ -34,7 +34,16 @@ def build(verbose: bool = False, sanitize: bool = False) -> str:
 
 
 def ensure_built() -> str:
-    """Build only when the shared object is missing or older than a source."""
+    """Build only when the shared object is missing or older than a source.
+
+    EAO_LIB, when set, names a library to load instead, built elsewhere from
+    a copy of the source (the mutation test plants one mistake in each copy
+    and runs the pins against it)."""
+    override = os.environ.get("EAO_LIB")
+    if override:
+        if not os.path.exists(override):
+            raise FileNotFoundError(f"EAO_LIB={override} does not exist")
+        return override
     sanitize = os.environ.get("EAO_SANITIZE") == "1"
     lib = SAN_LIB if sanitize else LIB
     if os.path.exists(lib):

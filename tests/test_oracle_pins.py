@@ -585,6 +585,29 @@ def test_error_feedback_off_keeps_no_residual():
         assert np.all(st.e_w == 0) and np.all(st.e_s == 0)
 
 
+def test_workers_compress_independently():
+    """Each worker compresses with randomness of its own, so the server's
+    average of N stochastic messages of one input deviates from it by about
+    1/N of one message's mean square error (identical draws on every worker
+    would leave the ratio at 1), and worker i draws the documented stream i."""
+    d, N = 4096, 8
+    q = q_(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, bucket=256)
+    cfg = O.Config(d=d, N=N, placement=O.ADAM_AT_SERVER, beta1=0.9, beta2=0.999, lr=1e-3, eps=1e-8,
+                   seed=5, qw=q, qs=q)
+    st = O.State.init(cfg, d)
+    g1 = np.random.default_rng(3).standard_normal(d).astype(np.float32)
+    out = O.step(cfg, 1, np.tile(g1, (N, 1)), st)
+    dw, _ = _dequant_msgs(cfg, out, d)
+    err = dw - g1.astype(np.float64)
+    one = np.mean(err ** 2)
+    avg = np.mean(err.mean(0) ** 2)
+    assert 0.6 / N < avg / one < 1.6 / N, avg / one
+    for i in range(N):
+        # at t = 1 with e_w = 0 the worker quantizes g itself
+        codes, _, _ = O.quantize(q, g1, u=O.uniforms(cfg.seed, 1, i, 0, d))
+        assert np.array_equal(O.unpack(2, out["wcodes"][i], d), codes), i
+
+
 # ---------------------------------------------------------------------------
 # Segments: the round is bucket-local, so a segment equals the same slice of
 # the full run (this is what makes sampled full-size parity possible).

@@ -128,3 +128,30 @@ def test_quantize_bucket_equals_quantize_under_its_own_scale():
         assert c.max() < 2 ** O.code_bits(q)
         if qd["kind"] == O.Q_SCALED_SIGN:
             assert np.all(np.abs(dq) == s2)
+
+
+@pytest.mark.parametrize("k_ex1", [1, 2, 3])
+def test_example1_under_a_smaller_scale_takes_the_nearest_level(k_ex1):
+    """Under a given scale below the bucket's max-norm (the tie check
+    quantizes under another side's scale), x/s leaves [-1, 1]; Example 1's Q2
+    still picks the nearest of its levels i/L, i = -L..L, which is +-1 beyond
+    them, so every code stays a level of M_2 and |Q(x)| <= s."""
+    rng = np.random.default_rng(k_ex1)
+    L = 2 ** k_ex1 - 1
+    kint = rng.integers(-64, 65, 256)
+    kint[0] = 64
+    p = kint.astype(np.float32)                     # max-norm 64
+    q = q_(O.Q_DET_UNIFORM, k_ex1 + 1, bucket=256)
+    s = 16.0                                        # x/s = k/16 exactly, up to 4
+    codes, deq = O.quantize_bucket(q, p, s)
+    assert codes.max() <= 2 * L and codes.min() >= 0
+    assert np.all(np.abs(deq) <= s)
+    for j in range(p.size):
+        x = Fraction(int(kint[j]), 16)
+        i = int(codes[j]) - L
+        best = min(abs(x - Fraction(m, L)) for m in range(-L, L + 1))
+        d = abs(x - Fraction(i, L))
+        # the exact nearest level, or at a half level the one nearer zero
+        assert d == best, (j, x, i)
+        if abs(x) > 1:
+            assert i == (L if x > 0 else -L)
