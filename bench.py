@@ -179,21 +179,35 @@ def paper_toy(args, E, allocate, init_state):
     step_args = rb.step_args()
     fused = args.call != "split"
 
-    def one(k):
+    def one(k, s):
         if fused:
             E.ea_toy_step(cfg, k + 1, A, xs, xi[k], rb.e_w, rb.m_w, rb.v_w, rb.m, rb.v, rb.e_s, rb.x, rb.wcodes,
-                          rb.scodes, gsq[k:k + 1], None, ws, stream=stream)
+                          rb.scodes, gsq[k:k + 1], None, ws, stream=s)
         else:
-            E.ea_toy_grad(d, N, A, xs, xi[k], rb.x, rb.g, gsq[k:k + 1], ws, stream=stream)
-            E.ea_step(cfg, k + 1, **step_args, stream=stream)
+            E.ea_toy_grad(d, N, A, xs, xi[k], rb.x, rb.g, gsq[k:k + 1], ws, stream=s)
+            E.ea_step(cfg, k + 1, **step_args, stream=s)
 
     for k in range(args.warmup):
-        one(k)
+        one(k, stream)
     torch.cuda.synchronize()
+    # A step is a few microseconds of GPU work, less than the host takes to
+    # issue it, so by default the timed steps are captured into one HIP graph
+    # (capture records the launches without running them) and replayed.
+    graph = None
+    if not args.eager:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cs = torch.cuda.current_stream()
+            for k in range(args.warmup, total):
+                one(k, cs)
+        torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record(stream)
-    for k in range(args.warmup, total):
-        one(k)
+    if graph is not None:
+        graph.replay()
+    else:
+        for k in range(args.warmup, total):
+            one(k, stream)
     stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
@@ -207,7 +221,8 @@ def paper_toy(args, E, allocate, init_state):
         "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": "paper_toy d=500 N=10 Example 2, Adam at the workers", "d": d, "N": N,
-                   "call": "ea_toy_step" if fused else "ea_toy_grad + ea_step"},
+                   "call": "ea_toy_step" if fused else "ea_toy_grad + ea_step",
+                   "launch": "eager" if args.eager else f"one HIP graph of the {args.steps} timed steps"},
         "roofline": {"bound": "hbm", "achieved": round(alg / (ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(alg / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 5), "traffic": None,
                      "kernel": ("toy residual + toy_round_kernel" if fused else "toy gradient kernels + step_kernel")
@@ -231,6 +246,9 @@ def main():
                          "replayed, or the four split calls (ea_worker_compress for each worker, "
                          "ea_server_aggregate_adam, ea_server_compress, ea_worker_apply)")
     ap.add_argument("--placement", default="server", choices=["server", "worker"])
+    ap.add_argument("--eager", action="store_true",
+                    help="paper_toy: issue every timed step from the host instead of replaying them "
+                         "from one HIP graph")
     ap.add_argument("--cpu-sample", type=int, default=1 << 24, help="parameters in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib-gib", type=float, default=0.0,

@@ -14,18 +14,24 @@
 // ea_toy_step, the gradient producer fused into the round (quantizers without
 // scales: Example 2, full precision), two launches:
 //   1. the residual, as above (which also clears the completion counter);
-//   2. toy_round_kernel: block b owns columns [64b, 64b+64), one per lane.
-//      Its 16 waves stage r - xi_i for a tile of rows of every worker in LDS
-//      and accumulate all workers' column sums (and the noise-free one) over
-//      contiguous row ranges, in binary64 with fused multiply-adds; the 16
-//      partial sums of an output are added in wave order.  Wave i then holds
+//   2. toy_round_kernel: block (b, r) owns columns [64b, 64b+64), one per
+//      lane, and the r-th of the splits of the rows of A.  Its 16 waves stage
+//      r - xi_i for a tile of rows of every worker in LDS and accumulate all
+//      workers' column sums (and the noise-free one) over contiguous row
+//      ranges, in binary64 with fused multiply-adds; the 16 partial sums of
+//      an output are added in wave order.  With several splits each block
+//      publishes its sums, and the last block of the column group to arrive
+//      adds the splits' sums in split order and goes on alone (no block
+//      waits for another); a small problem thereby spreads over many CUs
+//      instead of one block walking every row.  Wave i then holds
 //      worker i's gradient for the block's columns and runs its side of the
 //      round (Adam at the worker, the code, the residual); its codes fill a
 //      16-bit slice of each message word (the block's 64 elements are 16
 //      lanes of one 256-element chunk).  The last wave adds the workers'
 //      dequantized values in ascending order and runs the server side.  The
-//      gradient is never written to HBM.  The last block to finish adds the
-//      blocks' partial squared norms in block order.
+//      gradient is never written to HBM.  The last column group to finish adds
+//      the groups' partial squared norms (lane l those of groups l, l+64, ...,
+//      then the wave's sum).
 #include "ea_launch.hpp"
 
 namespace ea {
@@ -42,9 +48,11 @@ __global__ __launch_bounds__(kResWaves * kWave) void toy_residual_kernel(int64_t
                                                                          const float* __restrict__ xs,
                                                                          const float* __restrict__ x,
                                                                          double* __restrict__ res,
-                                                                         uint32_t* __restrict__ counter)
+                                                                         uint32_t* __restrict__ counter,
+                                                                         int32_t ncounter)
 {
-    if (counter != nullptr && blockIdx.x == 0 && threadIdx.x == 0) *counter = 0u;
+    if (counter != nullptr && blockIdx.x == 0)
+        for (int i = (int)threadIdx.x; i < ncounter; i += (int)blockDim.x) counter[i] = 0u;
     const int64_t k = (int64_t)blockIdx.x * kResWaves + threadIdx.x / kWave;
     if (k >= d) return;
     const int lane = lane_id();
@@ -127,8 +135,28 @@ __global__ __launch_bounds__(kWave) void toy_norm_kernel(int64_t nparts, const d
 constexpr int kTRWaves = 16;                   // waves per block
 constexpr int kTROut = 16;                     // column sums per pass: workers + the noise-free one
 constexpr int kTRWorkers = kTROut - 1;         // workers per pass
-constexpr int kTRRows = 256;                   // rows of A per staged tile
-constexpr int kTRPer = kTRRows / kTRWaves;     // rows of a tile per wave
+constexpr int kTRRows = 256;                   // rows of A per staged tile, one split
+constexpr int kTRSplitRows = 64;               // the same with several splits: one slot per thread
+constexpr int kTRMaxSplits = 8;                // splits of the rows per column group
+constexpr int kTRSplitBlocks = 1024;           // column groups x splits aimed at
+
+// Splits of the rows of A for d columns when the workers fit one pass (one
+// when the column groups alone fill the GPU), each a whole number of
+// kTRSplitRows tiles; `rows` receives the rows per split.
+int toy_splits(int64_t d, int64_t* rows)
+{
+    const int64_t nblk = (d + kWave - 1) / kWave;
+    int64_t R = (d + kTRSplitRows - 1) / kTRSplitRows;
+    if (R > kTRMaxSplits) R = kTRMaxSplits;
+    if (R > kTRSplitBlocks / nblk) R = kTRSplitBlocks / nblk;
+    if (R < 2) {
+        *rows = d;
+        return 1;
+    }
+    const int64_t per = (d + R - 1) / R;
+    *rows = (per + kTRSplitRows - 1) / kTRSplitRows * kTRSplitRows;
+    return (int)((d + *rows - 1) / *rows);
+}
 
 // Bits 0, 4, 8, ..., 60 of x gathered into bits 0..15.
 __device__ __forceinline__ uint32_t every_fourth_bit(uint64_t x)
@@ -194,16 +222,24 @@ struct ToyArgs {
     float *x, *e_w, *m_w, *v_w, *m, *v, *e_s;
     uint64_t *wcodes, *scodes;
     double* part;           // [blocks] partial squared norms of the noise-free gradient
-    uint32_t* counter;      // blocks done (cleared by the residual launch)
+    uint32_t* counter;      // [1 + blocks]: column groups done, then each group's splits
+                            // arrived (cleared by the residual launch)
+    int32_t splits;         // splits of the rows (gridDim.y); above 1 only with one pass
+    int64_t split_rows;     // rows per split
+    double* psum;           // [blocks][splits][kTROut][64] the splits' column sums
     double* grad_sq;        // nullable
     float* g_out;           // nullable: [N][d] the workers' gradients, for checking
 };
 
+template <int ROWS>
 __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
 {
+    constexpr int kPer = ROWS / kTRWaves;          // rows of a tile per wave
+    static_assert(ROWS % kTRWaves == 0 && ROWS * kTROut <= kTRWaves * kTROut * kWave, "tile shape");
     // Staged tiles (row-major [row][output]), then the waves' partial sums.
     __shared__ __attribute__((aligned(16))) double big[kTRWaves * kTROut * kWave];
     __shared__ float xfer[kTRWorkers * kWave];
+    __shared__ int last_split;
     const int lane = lane_id();
     const int w = (int)(threadIdx.x / kWave);
     const int64_t d = a.d;
@@ -241,17 +277,19 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
         double s[kTROut];
 #pragma unroll
         for (int o = 0; o < kTROut; ++o) s[o] = 0.0;
-        for (int64_t k0 = 0; k0 < d; k0 += kTRRows) {
-            const int rows = d - k0 < kTRRows ? (int)(d - k0) : kTRRows;
-            const int r0 = w * kTRPer;
-            float av[kTRPer];
+        const int64_t kb = (int64_t)blockIdx.y * a.split_rows;
+        const int64_t ke = d - kb < a.split_rows ? d : kb + a.split_rows;
+        for (int64_t k0 = kb; k0 < ke; k0 += ROWS) {
+            const int rows = ke - k0 < ROWS ? (int)(ke - k0) : ROWS;
+            const int r0 = w * kPer;
+            float av[kPer];
 #pragma unroll
-            for (int j = 0; j < kTRPer; ++j) av[j] = r0 + j < rows ? a.A[(k0 + r0 + j) * d + cc] : 0.0f;
+            for (int j = 0; j < kPer; ++j) av[j] = r0 + j < rows ? a.A[(k0 + r0 + j) * d + cc] : 0.0f;
             __syncthreads();                       // the previous tile has been read
             // every slot of the tile: outputs past nout and rows past the
             // tile's end hold zeros, so the sums below need no guards
-            for (int idx = threadIdx.x; idx < kTROut * kTRRows; idx += kTRWaves * kWave) {
-                const int o = idx / kTRRows, kk = idx - o * kTRRows;
+            for (int idx = threadIdx.x; idx < kTROut * ROWS; idx += kTRWaves * kWave) {
+                const int o = idx / ROWS, kk = idx - o * ROWS;
                 double val = 0.0;
                 if (kk < rows && o < nout) {
                     const double r = a.res[k0 + kk];
@@ -270,9 +308,9 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
                     s[2 * o2 + 1] = fma(ad, tv.y, s[2 * o2 + 1]);
                 }
             };
-            if (r0 + kTRPer <= rows) {
+            if (r0 + kPer <= rows) {
 #pragma unroll
-                for (int j = 0; j < kTRPer; ++j) row(j);
+                for (int j = 0; j < kPer; ++j) row(j);
             } else {
                 for (int j = 0; r0 + j < rows; ++j) row(j);
             }
@@ -282,9 +320,45 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
         for (int o = 0; o < kTROut; ++o)
             if (o < nout) big[(w * kTROut + o) * kWave + lane] = s[o];
         __syncthreads();
-        if (w < nout) {
-            double tot = 0.0;
+        double tot = 0.0;
+        if (w < nout)
             for (int u = 0; u < kTRWaves; ++u) tot += big[(u * kTROut + w) * kWave + lane];
+        if (a.splits > 1) {
+            // publish this split's sums; the group's last block adds them all
+            constexpr int64_t kSet = kTROut * kWave;
+            double* group = a.psum + (int64_t)blockIdx.x * a.splits * kSet;
+            // Each wave that stored releases its own stores (a write-back of
+            // the L2, no invalidation: the other blocks are still reading A
+            // through it); only the group's last block acquires.
+            if (w < nout) {
+                group[blockIdx.y * kSet + w * kWave + lane] = tot;
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                const bool last = atomicAdd(a.counter + 1 + blockIdx.x, 1u) == (uint32_t)(a.splits - 1);
+                if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                last_split = last ? 1 : 0;
+            }
+            __syncthreads();
+            if (!last_split) return;               // the whole block leaves together
+            if (w < nout) {
+                // all the loads first (one memory latency), then the sums in
+                // split order
+                const unsigned long long* bits = reinterpret_cast<const unsigned long long*>(group);
+                double part[kTRMaxSplits];
+#pragma unroll
+                for (int r = 0; r < kTRMaxSplits; ++r)
+                    part[r] = r < a.splits ? __longlong_as_double((long long)__atomic_load_n(
+                                                 bits + r * kSet + w * kWave + lane, __ATOMIC_RELAXED))
+                                           : 0.0;
+                tot = 0.0;
+#pragma unroll
+                for (int r = 0; r < kTRMaxSplits; ++r)
+                    if (r < a.splits) tot += part[r];
+            }
+        }
+        if (w < nout) {
             const double gd = 2.0 * tot;
             if (w < nw) {
                 // worker g0 + w (Algorithm 2 with Adam at the worker, else g + e)
@@ -309,21 +383,26 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
                 toy_store_codes(a.qw, a.wcodes + (int64_t)(g0 + w) * a.qw.words, col, in, code);
                 xfer[w * kWave + lane] = dq;
             } else if (a.grad_sq != nullptr) {
-                // the noise-free gradient: this block's share of ||grad F||^2;
-                // the last block to get here adds the shares in block order
+                // the noise-free gradient: this column group's share of
+                // ||grad F||^2; the last group to get here adds the shares:
+                // lane l the shares of groups l, l+64, ... in order (loaded
+                // side by side), then the wave's sum
                 const double sq = wave_sum(in ? gd * gd : 0.0);
+                uint32_t done = 0;
                 if (lane == 0) {
                     a.part[blockIdx.x] = sq;
-                    __threadfence();
-                    const uint32_t done = atomicAdd(a.counter, 1u);
-                    if (done == gridDim.x - 1) {
-                        __threadfence();
-                        double all = 0.0;
-                        const unsigned long long* bits = reinterpret_cast<const unsigned long long*>(a.part);
-                        for (uint32_t b = 0; b < gridDim.x; ++b)
-                            all += __longlong_as_double((long long)__atomic_load_n(bits + b, __ATOMIC_RELAXED));
-                        *a.grad_sq = all;
-                    }
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                    done = atomicAdd(a.counter, 1u);
+                    if (done == gridDim.x - 1) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                }
+                done = (uint32_t)__builtin_amdgcn_readfirstlane((int)done);
+                if (done == gridDim.x - 1) {
+                    double mine = 0.0;
+                    const unsigned long long* bits = reinterpret_cast<const unsigned long long*>(a.part);
+                    for (uint32_t b = (uint32_t)lane; b < gridDim.x; b += kWave)
+                        mine += __longlong_as_double((long long)__atomic_load_n(bits + b, __ATOMIC_RELAXED));
+                    const double all = wave_sum(mine);
+                    if (lane == 0) *a.grad_sq = all;
                 }
             }
         }
@@ -361,11 +440,16 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
 
 }  // namespace
 
-// r (d doubles), the per-block partial norms (one per 64 columns) and the
-// completion counter of the fused round.
+// r (d doubles), the per-block partial norms (one per 64 columns), the
+// fused round's counters (1 + one per column group, as 32-bit words) and its
+// splits' column sums.
 int64_t toy_workspace_bytes(int64_t d)
 {
-    return (d + (d + kWave - 1) / kWave + 1) * (int64_t)sizeof(double);
+    const int64_t nblk = (d + kWave - 1) / kWave;
+    int64_t rows = 0;
+    const int64_t R = toy_splits(d, &rows);
+    const int64_t psum = R > 1 ? nblk * R * kTROut * kWave : 0;
+    return (d + nblk + (nblk + 2) / 2 + psum) * (int64_t)sizeof(double);
 }
 
 hipError_t launch_toy_grad(int64_t d, int32_t N, const float* A, const float* xs, const float* xi, const float* x,
@@ -375,7 +459,7 @@ hipError_t launch_toy_grad(int64_t d, int32_t N, const float* A, const float* xs
     const int64_t ncol = (d + kWave - 1) / kWave;
     double* part = grad_sq ? res + d : nullptr;
     hipLaunchKernelGGL(toy_residual_kernel, dim3((unsigned)((d + kResWaves - 1) / kResWaves)),
-                       dim3(kResWaves * kWave), 0, s, d, A, xs, x, res, nullptr);
+                       dim3(kResWaves * kWave), 0, s, d, A, xs, x, res, nullptr, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(toy_columns_kernel, dim3((unsigned)ncol, (unsigned)((N + kToyWorkers - 1) / kToyWorkers)),
@@ -415,13 +499,22 @@ hipError_t launch_toy_step(const StepArgs& sa, const float* A, const float* xs, 
     a.scodes = sa.scodes;
     a.part = res + d;
     a.counter = reinterpret_cast<uint32_t*>(res + d + nblk);
+    a.psum = res + d + nblk + (nblk + 2) / 2;
     a.grad_sq = grad_sq;
     a.g_out = g_out;
+    // several splits only when the workers fit one pass (each pass would
+    // need its own sums) and the workspace holds them (toy_workspace_bytes)
+    a.splits = sa.N <= kTRWorkers ? toy_splits(d, &a.split_rows) : 1;
+    if (a.splits == 1) a.split_rows = d;
     hipLaunchKernelGGL(toy_residual_kernel, dim3((unsigned)((d + kResWaves - 1) / kResWaves)),
-                       dim3(kResWaves * kWave), 0, s, d, A, xs, sa.x, res, a.counter);
+                       dim3(kResWaves * kWave), 0, s, d, A, xs, sa.x, res, a.counter, (int32_t)(1 + nblk));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(toy_round_kernel, dim3((unsigned)nblk), dim3(kTRWaves * kWave), 0, s, a);
+    if (a.splits > 1)
+        hipLaunchKernelGGL(toy_round_kernel<kTRSplitRows>, dim3((unsigned)nblk, (unsigned)a.splits),
+                           dim3(kTRWaves * kWave), 0, s, a);
+    else
+        hipLaunchKernelGGL(toy_round_kernel<kTRRows>, dim3((unsigned)nblk), dim3(kTRWaves * kWave), 0, s, a);
     return hipGetLastError();
 }
 

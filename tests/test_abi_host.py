@@ -210,7 +210,12 @@ def test_toy_grad_rejected_before_device_work(E):
     assert E.lib.ea_toy_grad(500, 10, *p, P(4100), ws, None) == E.EA_ERR_ALIGN
     assert E.lib.ea_toy_grad(500, 10, *p, None, None, None) == E.EA_ERR_ARG
     assert E.lib.ea_toy_grad(500, 10, *p, None, P(4100), None) == E.EA_ERR_ALIGN
-    assert E.ea_toy_workspace_bytes(500) == 8 * (500 + 8 + 1)     # r, per-block norms, counter
+    # r, per-block norms, 1 + 8 counters (five doubles), and at d = 500 the
+    # fused round's row splits: 8 column groups x 8 splits of 64 rows, 16
+    # column sums of 64 columns each
+    assert E.ea_toy_workspace_bytes(500) == 8 * (500 + 8 + 5 + 8 * 8 * 16 * 64)
+    # the column groups alone fill the GPU: no splits
+    assert E.ea_toy_workspace_bytes(65536) == 8 * (65536 + 1024 + 513)
     with pytest.raises(E.EAError):
         E.ea_toy_workspace_bytes(0)
 

@@ -113,7 +113,7 @@ NONE = qfields(O.Q_NONE)
 FUSED = [(500, 10, EX2, O.ADAM_AT_WORKER), (500, 10, NONE, O.ADAM_AT_SERVER), (500, 10, EX2, O.ADAM_AT_SERVER),
          (64, 3, EX2, O.ADAM_AT_SERVER), (65, 1, EX2, O.ADAM_AT_WORKER), (1000, 17, EX2, O.ADAM_AT_WORKER),
          (777, 31, NONE, O.ADAM_AT_WORKER), (3000, 4, EX2, O.ADAM_AT_SERVER), (1, 2, EX2, O.ADAM_AT_WORKER),
-         (300, 15, EX2, O.ADAM_AT_WORKER), (300, 16, NONE, O.ADAM_AT_SERVER)]
+         (300, 15, EX2, O.ADAM_AT_WORKER), (300, 16, NONE, O.ADAM_AT_SERVER), (520, 6, EX2, O.ADAM_AT_SERVER)]
 
 
 def _ulps(a, b):
@@ -194,3 +194,53 @@ def test_toy_step_optional_outputs_change_nothing():
     torch.cuda.synchronize()
     for k in ("e_w", "m_w", "v_w", "e_s", "x", "wcodes", "scodes"):
         assert torch.equal(getattr(a, k).view(torch.uint8), getattr(b, k).view(torch.uint8)), k
+
+
+@pytest.mark.parametrize("d,N", [(500, 10), (300, 16)], ids=["split-rows", "one-split"])
+def test_toy_steps_replayed_from_a_graph(d, N):
+    """Five toy steps captured into a HIP graph (both launches of every step;
+    the round's counters are cleared by a kernel, not a memset) and replayed
+    three times from the same start, with eager resets and synchronizations
+    between the replays: every replay leaves the bits that the same five
+    steps leave when run eagerly."""
+    rng = np.random.default_rng(d + N)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    A = dev(rng.standard_normal((d, d)).astype(np.float32))
+    xs = dev((rng.standard_normal(d) * math.sqrt(0.1)).astype(np.float32))
+    xi = dev((rng.standard_normal((5, N, d)) * math.sqrt(0.1)).astype(np.float32))
+    _, ec = configs(d, N, EX2, EX2, O.ADAM_AT_WORKER, seed=9, beta1=0.9, beta2=0.99, lr=1e-4)
+    rb = allocate(ec)
+    init_state(ec, rb)
+    rb.x.copy_(dev((rng.standard_normal(d) * 0.01).astype(np.float32)))
+    keys = [k for k in ("e_w", "m_w", "v_w", "m", "v", "e_s", "x", "wcodes", "scodes") if getattr(rb, k) is not None]
+    start = {k: getattr(rb, k).clone() for k in keys}
+    gs = torch.zeros(5, dtype=torch.float64, device="cuda")
+    ws = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+
+    def steps():
+        for t in range(1, 6):
+            E.ea_toy_step(ec, t, A, xs, xi[t - 1], rb.e_w, rb.m_w, rb.v_w, rb.m, rb.v, rb.e_s, rb.x, rb.wcodes,
+                          rb.scodes, gs[t - 1:t], None, ws)
+
+    def reset():
+        for k in keys:
+            getattr(rb, k).copy_(start[k])
+        gs.zero_()
+        torch.cuda.synchronize()
+
+    steps()
+    torch.cuda.synchronize()
+    want = {k: getattr(rb, k).clone() for k in keys}
+    want_gs = gs.clone()
+    reset()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        steps()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        reset()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k in keys:
+            assert torch.equal(getattr(rb, k).view(torch.uint8), want[k].view(torch.uint8)), (rep, k)
+        assert torch.equal(gs, want_gs), rep
