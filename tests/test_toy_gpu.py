@@ -113,7 +113,8 @@ NONE = qfields(O.Q_NONE)
 FUSED = [(500, 10, EX2, O.ADAM_AT_WORKER), (500, 10, NONE, O.ADAM_AT_SERVER), (500, 10, EX2, O.ADAM_AT_SERVER),
          (64, 3, EX2, O.ADAM_AT_SERVER), (65, 1, EX2, O.ADAM_AT_WORKER), (1000, 17, EX2, O.ADAM_AT_WORKER),
          (777, 31, NONE, O.ADAM_AT_WORKER), (3000, 4, EX2, O.ADAM_AT_SERVER), (1, 2, EX2, O.ADAM_AT_WORKER),
-         (300, 15, EX2, O.ADAM_AT_WORKER), (300, 16, NONE, O.ADAM_AT_SERVER), (520, 6, EX2, O.ADAM_AT_SERVER)]
+         (300, 15, EX2, O.ADAM_AT_WORKER), (300, 16, NONE, O.ADAM_AT_SERVER), (520, 6, EX2, O.ADAM_AT_SERVER),
+         (4096, 3, EX2, O.ADAM_AT_WORKER)]
 
 
 def _ulps(a, b):
