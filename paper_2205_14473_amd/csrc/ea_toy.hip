@@ -9,7 +9,8 @@
 //      block take 16 contiguous ranges of k, their partial sums meet in LDS
 //      and are added in wave order; block (b, 0) also forms the noise-free
 //      gradient and the partial sum of its squares for its columns;
-//   3. norm: the per-block partial sums added in block order.
+//   3. norm: the per-block partial sums added by one wave (lane l those of
+//      blocks l, l+64, ..., then the wave's sum).
 //
 // ea_toy_step, the gradient producer fused into the round (quantizers without
 // scales: Example 2, full precision), two launches:
@@ -122,10 +123,12 @@ __global__ __launch_bounds__(kColThreads) void toy_columns_kernel(int64_t d, int
 __global__ __launch_bounds__(kWave) void toy_norm_kernel(int64_t nparts, const double* __restrict__ part,
                                                          double* __restrict__ grad_sq)
 {
-    if (threadIdx.x != 0) return;
+    // lane l adds the parts l, l+64, ... in order, then the wave's sum
+    const int lane = lane_id();
     double s = 0.0;
-    for (int64_t b = 0; b < nparts; ++b) s += part[b];
-    *grad_sq = s;
+    for (int64_t b = lane; b < nparts; b += kWave) s += part[b];
+    s = wave_sum(s);
+    if (lane == 0) *grad_sq = s;
 }
 
 
