@@ -320,9 +320,9 @@ int ea_toy_grad(int64_t d, int32_t N, const float *A, const float *x_star, const
  *   scodes as ea_step (no scales); grad_sq (device, one double, write, or
  *   NULL); g_out (device, N*d, write, or NULL); workspace (device,
  *   ea_toy_workspace_bytes(d) bytes, 8-byte aligned).
- *   The gradients' products are summed in binary64 (in another order than
- *   ea_toy_grad's, with fused multiply-adds) and each g_i rounded once to
- *   binary32.  1 <= d <= 65536, 1 <= N <= 1024, 1 <= t <= 2^32-1. */
+ *   The gradients' products are summed in binary64 (with fused multiply-adds,
+ *   in the same order as ea_toy_grad's, whose gradients equal these bit for
+ *   bit) and each g_i rounded once to binary32.  1 <= d <= 65536, 1 <= N <= 1024, 1 <= t <= 2^32-1. */
 int ea_toy_step(const ea_config_t *c, int64_t t, const float *A, const float *x_star, const float *xi, float *e_w,
                 float *m_w, float *v_w, float *m, float *v, float *e_s, float *x, uint64_t *wcodes,
                 uint64_t *scodes, double *grad_sq, float *g_out, void *workspace, void *stream);

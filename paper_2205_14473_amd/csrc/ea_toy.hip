@@ -3,18 +3,9 @@
 // g_i = 2 A^T (A x - x* - xi_i).  Products are summed in binary64 and each g
 // rounded once to binary32, like the oracle.
 //
-// ea_toy_grad, three launches:
-//   1. residual: res[k] = (A x)[k] - x*[k], one wave per row of A;
-//   2. columns:  blocks of 64 columns x up to 8 workers; the 16 waves of a
-//      block take 16 contiguous ranges of k, their partial sums meet in LDS
-//      and are added in wave order; block (b, 0) also forms the noise-free
-//      gradient and the partial sum of its squares for its columns;
-//   3. norm: the per-block partial sums added by one wave (lane l those of
-//      blocks l, l+64, ..., then the wave's sum).
-//
-// ea_toy_step, the gradient producer fused into the round (quantizers without
-// scales: Example 2, full precision), two launches:
-//   1. the residual, as above (which also clears the completion counter);
+// Two launches for both entry points:
+//   1. residual: res[k] = (A x)[k] - x*[k], one wave per row of A (it also
+//      clears the counters of the second launch);
 //   2. toy_round_kernel: block (b, r) owns columns [64b, 64b+64), one per
 //      lane, and the r-th of the splits of the rows of A.  Its 16 waves stage
 //      r - xi_i for a tile of rows of every worker in LDS and accumulate all
@@ -24,15 +15,19 @@
 //      publishes its sums, and the last block of the column group to arrive
 //      adds the splits' sums in split order and goes on alone (no block
 //      waits for another); a small problem thereby spreads over many CUs
-//      instead of one block walking every row.  Wave i then holds
-//      worker i's gradient for the block's columns and runs its side of the
-//      round (Adam at the worker, the code, the residual); its codes fill a
-//      16-bit slice of each message word (the block's 64 elements are 16
-//      lanes of one 256-element chunk).  The last wave adds the workers'
-//      dequantized values in ascending order and runs the server side.  The
-//      gradient is never written to HBM.  The last column group to finish adds
-//      the groups' partial squared norms (lane l those of groups l, l+64, ...,
-//      then the wave's sum).
+//      instead of one block walking every row.  The last column group to
+//      finish adds the groups' partial squared norms of the noise-free
+//      gradient (lane l those of groups l, l+64, ..., then the wave's sum).
+//
+// ea_toy_grad writes the gradients and stops there.  ea_toy_step fuses the
+// producer into the round (quantizers without scales: Example 2, full
+// precision): wave i holds worker i's gradient for the block's columns and
+// runs its side of the round (Adam at the worker, the code, the residual);
+// its codes fill a 16-bit slice of each message word (the block's 64
+// elements are 16 lanes of one 256-element chunk).  The last wave adds the
+// workers' dequantized values in ascending order and runs the server side.
+// The gradient is not written to HBM unless asked for (g_out).  Both entry
+// points sum in the same order, so their gradients agree bit for bit.
 #include "ea_launch.hpp"
 
 namespace ea {
@@ -40,10 +35,6 @@ namespace ea {
 namespace {
 
 constexpr int kResWaves = 4;                    // rows per residual block
-constexpr int kColThreads = 1024;
-constexpr int kColWaves = kColThreads / kWave;
-constexpr int kToyWorkers = 8;                  // workers per column block
-constexpr int kToyOut = kToyWorkers + 1;        // + the noise-free gradient
 
 __global__ __launch_bounds__(kResWaves * kWave) void toy_residual_kernel(int64_t d, const float* __restrict__ A,
                                                                          const float* __restrict__ xs,
@@ -72,65 +63,6 @@ __global__ __launch_bounds__(kResWaves * kWave) void toy_residual_kernel(int64_t
     s = wave_sum(s);
     if (lane == 0) res[k] = s - (double)xs[k];
 }
-
-__global__ __launch_bounds__(kColThreads) void toy_columns_kernel(int64_t d, int32_t N, const float* __restrict__ A,
-                                                                 const double* __restrict__ res,
-                                                                 const float* __restrict__ xi,
-                                                                 float* __restrict__ g, double* __restrict__ part)
-{
-    __shared__ double sums[kColWaves][kToyOut][kWave];
-    const int lane = lane_id();
-    const int w = (int)(threadIdx.x / kWave);
-    const int64_t j = (int64_t)blockIdx.x * kWave + lane;
-    const int i0 = (int)blockIdx.y * kToyWorkers;
-    const int W = N - i0 < kToyWorkers ? N - i0 : kToyWorkers;
-    const bool full = blockIdx.y == 0 && part != nullptr;
-    const int64_t per = (d + kColWaves - 1) / kColWaves;
-    const int64_t k0 = (int64_t)w * per;
-    const int64_t k1 = k0 + per < d ? k0 + per : d;
-
-    double acc[kToyOut];
-#pragma unroll
-    for (int c = 0; c < kToyOut; ++c) acc[c] = 0.0;
-    if (j < d) {
-#pragma unroll 4
-        for (int64_t k = k0; k < k1; ++k) {
-            const double a = (double)A[k * d + j];
-            const double r0 = res[k];
-            if (full) acc[0] += a * r0;
-#pragma unroll
-            for (int c = 0; c < kToyWorkers; ++c)
-                if (c < W) acc[c + 1] += a * (r0 - (double)xi[(int64_t)(i0 + c) * d + k]);
-        }
-    }
-#pragma unroll
-    for (int c = 0; c < kToyOut; ++c) sums[w][c][lane] = acc[c];
-    __syncthreads();
-    if (w > W) return;
-    double s = 0.0;
-    for (int u = 0; u < kColWaves; ++u) s += sums[u][w][lane];
-    if (w > 0) {
-        if (j < d) g[(int64_t)(i0 + w - 1) * d + j] = (float)(2.0 * s);
-        return;
-    }
-    if (!full) return;
-    const double gj = 2.0 * s;
-    double sq = j < d ? gj * gj : 0.0;
-    sq = wave_sum(sq);
-    if (lane == 0) part[blockIdx.x] = sq;
-}
-
-__global__ __launch_bounds__(kWave) void toy_norm_kernel(int64_t nparts, const double* __restrict__ part,
-                                                         double* __restrict__ grad_sq)
-{
-    // lane l adds the parts l, l+64, ... in order, then the wave's sum
-    const int lane = lane_id();
-    double s = 0.0;
-    for (int64_t b = lane; b < nparts; b += kWave) s += part[b];
-    s = wave_sum(s);
-    if (lane == 0) *grad_sq = s;
-}
-
 
 // ---------------------------------------------------------------------------
 // The fused toy round.
@@ -234,7 +166,9 @@ struct ToyArgs {
     float* g_out;           // nullable: [N][d] the workers' gradients, for checking
 };
 
-template <int ROWS>
+// ROUND: the round follows the gradients; without it the kernel only writes
+// the gradients to g_out (ea_toy_grad) and the norm.
+template <int ROWS, bool ROUND>
 __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
 {
     constexpr int kPer = ROWS / kTRWaves;          // rows of a tile per wave
@@ -254,7 +188,7 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
     float acc = 0.0f;                              // the server wave's sum of dequantized messages
     // the server's rows of the block's columns (only this block writes them)
     float sm = 0.0f, sv = 0.0f, se = 0.0f, sx = 0.0f;
-    if (w == kServer && in) {
+    if (ROUND && w == kServer && in) {
         if (!atw) {
             sm = a.m[col];
             sv = a.v[col];
@@ -270,7 +204,7 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
         // the worker's rows, loaded now so that they arrive during the sums
         const int64_t wrow = (int64_t)(g0 + (w < nw ? w : 0)) * d + cc;
         float e0 = 0.0f, m0 = 0.0f, v0 = 0.0f;
-        if (w < nw) {
+        if (ROUND && w < nw) {
             e0 = a.e_w[wrow];
             if (atw) {
                 m0 = a.m_w[wrow];
@@ -367,24 +301,26 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
                 // worker g0 + w (Algorithm 2 with Adam at the worker, else g + e)
                 const float g = (float)gd;
                 if (a.g_out != nullptr && in) a.g_out[wrow] = g;
-                float p;
-                if (atw) {
-                    const float vk = a.beta2 * v0 + (1.0f - a.beta2) * (g * g);
-                    const float mk = a.beta1 * m0 + (1.0f - a.beta1) * g;
-                    p = (vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f) + e0;
-                    if (in) {
-                        a.m_w[wrow] = mk;
-                        a.v_w[wrow] = vk;
+                if constexpr (ROUND) {
+                    float p;
+                    if (atw) {
+                        const float vk = a.beta2 * v0 + (1.0f - a.beta2) * (g * g);
+                        const float mk = a.beta1 * m0 + (1.0f - a.beta1) * g;
+                        p = (vk > 0.0f ? a.lr * (mk / sqrtf(vk)) : 0.0f) + e0;
+                        if (in) {
+                            a.m_w[wrow] = mk;
+                            a.v_w[wrow] = vk;
+                        }
+                    } else {
+                        p = g + e0;
                     }
-                } else {
-                    p = g + e0;
+                    uint32_t code;
+                    float dq;
+                    toy_code(a.qw, p, code, dq);
+                    if (in) a.e_w[wrow] = a.qw.ef ? p - dq : 0.0f;
+                    toy_store_codes(a.qw, a.wcodes + (int64_t)(g0 + w) * a.qw.words, col, in, code);
+                    xfer[w * kWave + lane] = dq;
                 }
-                uint32_t code;
-                float dq;
-                toy_code(a.qw, p, code, dq);
-                if (in) a.e_w[wrow] = a.qw.ef ? p - dq : 0.0f;
-                toy_store_codes(a.qw, a.wcodes + (int64_t)(g0 + w) * a.qw.words, col, in, code);
-                xfer[w * kWave + lane] = dq;
             } else if (a.grad_sq != nullptr) {
                 // the noise-free gradient: this column group's share of
                 // ||grad F||^2; the last group to get here adds the shares:
@@ -410,11 +346,11 @@ __global__ __launch_bounds__(kTRWaves * kWave) void toy_round_kernel(ToyArgs a)
             }
         }
         __syncthreads();
-        if (w == kServer)
+        if (ROUND && w == kServer)
             for (int i = 0; i < nw; ++i) acc = acc + xfer[i * kWave + lane];
     }
 
-    if (w == kServer) {
+    if (ROUND && w == kServer) {
         // Algorithm 1: average, [Adam at the server], residual, quantize, apply
         const float fN = (float)a.N;
         const bool pow2 = (a.N & (a.N - 1)) == 0;
@@ -455,32 +391,57 @@ int64_t toy_workspace_bytes(int64_t d)
     return (d + nblk + (nblk + 2) / 2 + psum) * (int64_t)sizeof(double);
 }
 
+namespace {
+
+// The residual launch (which also clears the counters), then the round
+// kernel, with the round (ROUND) or writing the gradients only.
+template <bool ROUND>
+hipError_t launch_toy(ToyArgs& a, const float* xs, const float* x, void* workspace, hipStream_t s)
+{
+    const int64_t d = a.d;
+    const int64_t nblk = (d + kWave - 1) / kWave;
+    double* res = static_cast<double*>(workspace);
+    a.res = res;
+    a.part = res + d;
+    a.counter = reinterpret_cast<uint32_t*>(res + d + nblk);
+    a.psum = res + d + nblk + (nblk + 2) / 2;
+    // several splits only when the workers fit one pass (each pass would
+    // need its own sums) and the workspace holds them (toy_workspace_bytes)
+    a.splits = a.N <= kTRWorkers ? toy_splits(d, &a.split_rows) : 1;
+    if (a.splits == 1) a.split_rows = d;
+    hipLaunchKernelGGL(toy_residual_kernel, dim3((unsigned)((d + kResWaves - 1) / kResWaves)),
+                       dim3(kResWaves * kWave), 0, s, d, a.A, xs, x, res, a.counter, (int32_t)(1 + nblk));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (a.splits > 1)
+        hipLaunchKernelGGL((toy_round_kernel<kTRSplitRows, ROUND>), dim3((unsigned)nblk, (unsigned)a.splits),
+                           dim3(kTRWaves * kWave), 0, s, a);
+    else
+        hipLaunchKernelGGL((toy_round_kernel<kTRRows, ROUND>), dim3((unsigned)nblk), dim3(kTRWaves * kWave), 0, s,
+                           a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_toy_grad(int64_t d, int32_t N, const float* A, const float* xs, const float* xi, const float* x,
                            float* g, double* grad_sq, void* workspace, hipStream_t s)
 {
-    double* res = static_cast<double*>(workspace);
-    const int64_t ncol = (d + kWave - 1) / kWave;
-    double* part = grad_sq ? res + d : nullptr;
-    hipLaunchKernelGGL(toy_residual_kernel, dim3((unsigned)((d + kResWaves - 1) / kResWaves)),
-                       dim3(kResWaves * kWave), 0, s, d, A, xs, x, res, nullptr, 0);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(toy_columns_kernel, dim3((unsigned)ncol, (unsigned)((N + kToyWorkers - 1) / kToyWorkers)),
-                       dim3(kColThreads), 0, s, d, N, A, res, xi, g, part);
-    e = hipGetLastError();
-    if (e != hipSuccess || !grad_sq) return e;
-    hipLaunchKernelGGL(toy_norm_kernel, dim3(1), dim3(kWave), 0, s, ncol, part, grad_sq);
-    return hipGetLastError();
+    ToyArgs a{};
+    a.d = d;
+    a.N = N;
+    a.A = A;
+    a.xi = xi;
+    a.g_out = g;
+    a.grad_sq = grad_sq;
+    return launch_toy<false>(a, xs, x, workspace, s);
 }
 
 hipError_t launch_toy_step(const StepArgs& sa, const float* A, const float* xs, const float* xi, double* grad_sq,
                            float* g_out, void* workspace, hipStream_t s)
 {
-    const int64_t d = sa.d;
-    const int64_t nblk = (d + kWave - 1) / kWave;
-    double* res = static_cast<double*>(workspace);
     ToyArgs a{};
-    a.d = d;
+    a.d = sa.d;
     a.N = sa.N;
     a.placement = sa.placement;
     a.beta1 = sa.beta1;
@@ -489,7 +450,6 @@ hipError_t launch_toy_step(const StepArgs& sa, const float* A, const float* xs, 
     a.qw = sa.qw;
     a.qs = sa.qs;
     a.A = A;
-    a.res = res;
     a.xi = xi;
     a.x = sa.x;
     a.e_w = sa.e_w;
@@ -500,25 +460,9 @@ hipError_t launch_toy_step(const StepArgs& sa, const float* A, const float* xs, 
     a.e_s = sa.e_s;
     a.wcodes = sa.wcodes;
     a.scodes = sa.scodes;
-    a.part = res + d;
-    a.counter = reinterpret_cast<uint32_t*>(res + d + nblk);
-    a.psum = res + d + nblk + (nblk + 2) / 2;
     a.grad_sq = grad_sq;
     a.g_out = g_out;
-    // several splits only when the workers fit one pass (each pass would
-    // need its own sums) and the workspace holds them (toy_workspace_bytes)
-    a.splits = sa.N <= kTRWorkers ? toy_splits(d, &a.split_rows) : 1;
-    if (a.splits == 1) a.split_rows = d;
-    hipLaunchKernelGGL(toy_residual_kernel, dim3((unsigned)((d + kResWaves - 1) / kResWaves)),
-                       dim3(kResWaves * kWave), 0, s, d, A, xs, sa.x, res, a.counter, (int32_t)(1 + nblk));
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if (a.splits > 1)
-        hipLaunchKernelGGL(toy_round_kernel<kTRSplitRows>, dim3((unsigned)nblk, (unsigned)a.splits),
-                           dim3(kTRWaves * kWave), 0, s, a);
-    else
-        hipLaunchKernelGGL(toy_round_kernel<kTRRows>, dim3((unsigned)nblk), dim3(kTRWaves * kWave), 0, s, a);
-    return hipGetLastError();
+    return launch_toy<true>(a, xs, sa.x, workspace, s);
 }
 
 }  // namespace ea

@@ -245,3 +245,24 @@ def test_toy_steps_replayed_from_a_graph(d, N):
         for k in keys:
             assert torch.equal(getattr(rb, k).view(torch.uint8), want[k].view(torch.uint8)), (rep, k)
         assert torch.equal(gs, want_gs), rep
+
+
+@pytest.mark.parametrize("d,N", [(500, 10), (777, 31), (65, 2)], ids=["split-rows", "two-passes", "ragged"])
+def test_toy_grad_equals_fused_step_gradients(d, N):
+    """ea_toy_grad and ea_toy_step (through g_out) sum in the same order: the
+    same gradients bit for bit, and the same ||grad F||^2."""
+    A, xs, xi, x = _inputs(d, N, 11)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    g, gs = _gpu_grad(A, xs, xi, x)
+    _, ec = configs(d, N, EX2, EX2, O.ADAM_AT_WORKER, seed=9, beta1=0.9, beta2=0.99, lr=1e-4)
+    rb = allocate(ec)
+    init_state(ec, rb)
+    rb.x.copy_(dev(x))
+    g2 = torch.empty((N, d), dtype=torch.float32, device="cuda")
+    gs2 = torch.zeros(1, dtype=torch.float64, device="cuda")
+    ws = torch.empty(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+    E.ea_toy_step(ec, 1, dev(A), dev(xs), dev(xi), rb.e_w, rb.m_w, rb.v_w, rb.m, rb.v, rb.e_s, rb.x, rb.wcodes,
+                  rb.scodes, gs2, g2, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(g.view(np.uint32), g2.cpu().numpy().view(np.uint32))
+    assert gs == float(gs2.item())
