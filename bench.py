@@ -157,8 +157,10 @@ def paper_toy(args, E, allocate, init_state):
     gradient producer fused into the round: two launches, the gradients never
     leave the chip); --call split times ea_toy_grad followed by ea_step.  The
     noise draws of all steps are generated before the timed region.  The
-    problem lives in cache and is bound by launch latency and the binary64
-    sums, so the roofline fraction is reported for completeness."""
+    problem lives in cache and is bound by the latency of its dependent
+    memory trips (a few microseconds of GPU work per step, less than the
+    host takes to issue it, hence the graph), so the roofline fraction is
+    reported for completeness."""
     import torch
     toy = W.PAPER_TOY
     d, N = toy["d"], toy["N"]
@@ -225,8 +227,9 @@ def paper_toy(args, E, allocate, init_state):
                    "launch": "eager" if args.eager else f"one HIP graph of the {args.steps} timed steps"},
         "roofline": {"bound": "hbm", "achieved": round(alg / (ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(alg / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 5), "traffic": None,
-                     "kernel": ("toy residual + toy_round_kernel" if fused else "toy gradient kernels + step_kernel")
-                     + " (cache-resident; launch-bound)"},
+                     "kernel": ("toy residual + toy_round_kernel" if fused
+                                else "toy residual + toy_round_kernel (gradients only) + step_kernel")
+                     + " (cache-resident; bound by dependent memory latency)"},
         "grad_sq_first_last": [float(g[0]), float(g[-1])],
     }
     print(json.dumps(line), flush=True)
