@@ -158,9 +158,7 @@ def paper_toy(args, E, allocate, init_state):
     leave the chip); --call split times ea_toy_grad followed by ea_step.  The
     noise draws of all steps are generated before the timed region.  The
     problem lives in cache and is bound by the latency of its dependent
-    memory trips (a few microseconds of GPU work per step, less than the
-    host takes to issue it, hence the graph), so the roofline fraction is
-    reported for completeness."""
+    memory trips, so the roofline fraction is reported for completeness."""
     import torch
     toy = W.PAPER_TOY
     d, N = toy["d"], toy["N"]
@@ -192,9 +190,10 @@ def paper_toy(args, E, allocate, init_state):
     for k in range(args.warmup):
         one(k, stream)
     torch.cuda.synchronize()
-    # A step is a few microseconds of GPU work, less than the host takes to
-    # issue it, so by default the timed steps are captured into one HIP graph
-    # (capture records the launches without running them) and replayed.
+    # A step is about 20 us of GPU work, close to what the host takes to
+    # issue it from Python, so by default the timed steps are captured into
+    # one HIP graph (capture records the launches without running them) and
+    # replayed: the time is then the GPU's alone.
     graph = None
     if not args.eager:
         graph = torch.cuda.CUDAGraph()
