@@ -1,0 +1,115 @@
+"""Writes stay inside the buffers the header sizes: every array an entry point
+writes (state, messages, scales, workspace) is placed at the front of a
+larger allocation filled with a byte pattern, and after the calls every byte
+past the array's end still holds the pattern.  The configurations cover a
+ragged last tile, two-tile blocks, 8-chunk tiles, whole-vector scales (the
+workspace's partial sums), sparse messages, raw messages, the no-allocation
+round and the toy problem's split-row workspace."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU-only host
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2205_14473_amd as E  # noqa: E402
+from paper_2205_14473_amd.state import allocate, init_state  # noqa: E402
+from parity_util import configs, qfields  # noqa: E402
+
+GUARD = 4096
+PATTERN = 0xA5
+
+
+class Guarded:
+    """Tensors viewed from the front of larger pattern-filled allocations."""
+
+    def __init__(self):
+        self.bufs = {}
+
+    def wrap(self, name, t):
+        if t is None:
+            return None
+        nbytes = t.numel() * t.element_size()
+        big = torch.full((nbytes + GUARD,), PATTERN, dtype=torch.uint8, device="cuda")
+        view = big[:nbytes].view(t.dtype).view(t.shape)
+        view.copy_(t)
+        self.bufs[name] = (big, nbytes)
+        return view
+
+    def check(self, what):
+        torch.cuda.synchronize()
+        for name, (big, nbytes) in self.bufs.items():
+            tail = big[nbytes:]
+            bad = int((tail != PATTERN).sum().item())
+            assert bad == 0, f"{what}: {bad} bytes written past the end of {name} ({nbytes} bytes)"
+
+
+def _step_args(ec, rb, gd):
+    args = rb.step_args()
+    nsw, nss = E.ea_msg_scales(ec.qw, ec.d), E.ea_msg_scales(ec.qs, ec.d)
+    args["wscales"] = args["wscales"][:, :nsw] if nsw else None
+    args["sscales"] = args["sscales"][:nss] if nss else None
+    out = {}
+    for k, t in args.items():
+        out[k] = gd.wrap(k, t.contiguous() if t is not None else None)
+    return out
+
+
+ROUNDS = [
+    ("stoch4-ragged", 5000, 3, qfields(O.Q_STOCH_UNIFORM, 4, O.SCALE_L2, bucket=512), O.ADAM_AT_SERVER),
+    ("sign-global-worker", 3001, 5, qfields(O.Q_SCALED_SIGN, 1, bucket=0), O.ADAM_AT_WORKER),
+    ("topk", 2500, 4, dict(kind=O.Q_TOPK, keep=16, bucket=512, error_feedback=1), O.ADAM_AT_SERVER),
+    ("ex1-wide", 777, 17, qfields(O.Q_DET_UNIFORM, 3, bucket=2048), O.ADAM_AT_SERVER),
+    ("stoch2-max-wide", 9000, 8, qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, bucket=2048), O.ADAM_AT_WORKER),
+    ("raw", 1000, 2, qfields(O.Q_NONE), O.ADAM_AT_SERVER),
+    ("randk-short-bucket", 1500, 3, dict(kind=O.Q_RANDK, keep=40, bucket=2048, error_feedback=1), O.ADAM_AT_WORKER),
+]
+
+
+@pytest.mark.parametrize("name,d,N,q,placement", ROUNDS, ids=[r[0] for r in ROUNDS])
+@pytest.mark.parametrize("call", ["step", "noalloc"])
+def test_round_writes_stay_in_bounds(name, d, N, q, placement, call):
+    _, ec = configs(d, N, q, q, placement, seed=3)
+    rb = allocate(ec)
+    init_state(ec, rb)
+    rng = np.random.default_rng(d + N)
+    rb.g.copy_(torch.from_numpy((rng.standard_normal((N, d)) * 1e-2).astype(np.float32)))
+    gd = Guarded()
+    args = _step_args(ec, rb, gd)
+    for t in (1, 2):
+        if call == "step":
+            E.ea_step(ec, t, **args)
+        else:
+            a = dict(args)
+            a.pop("workspace")
+            E.ea_step_noalloc(ec, t, **a)
+    gd.check(f"{call} {name}")
+
+
+@pytest.mark.parametrize("d,N", [(500, 10), (65, 2), (777, 31), (4096, 3)])
+def test_toy_writes_stay_in_bounds(d, N):
+    rng = np.random.default_rng(d)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    A = dev(rng.standard_normal((d, d)).astype(np.float32))
+    xs = dev((rng.standard_normal(d) * math.sqrt(0.1)).astype(np.float32))
+    xi = dev((rng.standard_normal((N, d)) * math.sqrt(0.1)).astype(np.float32))
+    ex2 = qfields(O.Q_POW2, kmin=-17, kmax=-11)
+    _, ec = configs(d, N, ex2, ex2, O.ADAM_AT_WORKER, seed=9, beta1=0.9, beta2=0.99, lr=1e-4)
+    rb = allocate(ec)
+    init_state(ec, rb)
+    gd = Guarded()
+    st = {k: gd.wrap(k, getattr(rb, k)) for k in ("e_w", "m_w", "v_w", "e_s", "x", "wcodes", "scodes")}
+    ws = gd.wrap("workspace", torch.zeros(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda"))
+    g = gd.wrap("g", torch.zeros((N, d), dtype=torch.float32, device="cuda"))
+    gs = gd.wrap("grad_sq", torch.zeros(1, dtype=torch.float64, device="cuda"))
+    for t in (1, 2):
+        E.ea_toy_step(ec, t, A, xs, xi, st["e_w"], st["m_w"], st["v_w"], None, None, st["e_s"], st["x"],
+                      st["wcodes"], st["scodes"], gs, g, ws)
+    E.ea_toy_grad(d, N, A, xs, xi, st["x"], g, gs, ws)
+    gd.check(f"toy d={d} N={N}")
