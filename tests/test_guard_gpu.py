@@ -1,5 +1,7 @@
 """Writes stay inside the buffers the header sizes: every array an entry point
-writes (state, messages, scales, workspace) is placed at the front of a
+(the round, the no-allocation round, the scheduled round and the multi-step
+run, the four split calls, the toy calls) writes (state, messages, scales,
+workspace, the step counter) is placed at the front of a
 larger allocation filled with a byte pattern, and after the calls every byte
 past the array's end still holds the pattern.  The configurations cover a
 ragged last tile, two-tile blocks, 8-chunk tiles, whole-vector scales (the
@@ -73,23 +75,70 @@ ROUNDS = [
 
 
 @pytest.mark.parametrize("name,d,N,q,placement", ROUNDS, ids=[r[0] for r in ROUNDS])
-@pytest.mark.parametrize("call", ["step", "noalloc"])
+@pytest.mark.parametrize("call", ["step", "noalloc", "scheduled", "run", "split"])
 def test_round_writes_stay_in_bounds(name, d, N, q, placement, call):
     _, ec = configs(d, N, q, q, placement, seed=3)
-    rb = allocate(ec)
+    rb = allocate(ec, with_u=True)
     init_state(ec, rb)
     rng = np.random.default_rng(d + N)
     rb.g.copy_(torch.from_numpy((rng.standard_normal((N, d)) * 1e-2).astype(np.float32)))
     gd = Guarded()
+    sched = E.Schedule(kind=E.EA_SCHED_STEP_DECAY, alpha=1e-3, factor=0.5, period=1)
+    if call == "split":
+        _split_rounds(ec, rb, gd)
+        gd.check(f"split {name}")
+        return
     args = _step_args(ec, rb, gd)
+    if call == "run":
+        a = dict(args)
+        g = a.pop("g")
+        E.ea_run(ec, sched, 1, 2, g, 0, **a)
+    elif call == "scheduled":
+        t_dev = gd.wrap("t_dev", torch.ones(1, dtype=torch.int32, device="cuda"))
+        for _ in range(2):
+            E.ea_step_scheduled(ec, sched, t_dev, **args)
     for t in (1, 2):
         if call == "step":
             E.ea_step(ec, t, **args)
-        else:
+        elif call == "noalloc":
             a = dict(args)
             a.pop("workspace")
             E.ea_step_noalloc(ec, t, **a)
     gd.check(f"{call} {name}")
+
+
+def _split_rounds(ec, rb, gd):
+    """Two rounds through the four split calls.  Each worker's rows and
+    message sit in allocations of their own, so that a worker call writing
+    past its row is caught (the next worker would overwrite it in a shared
+    array); the server calls get the workers' messages side by side, as they
+    take them."""
+    d, N = ec.d, ec.N
+    nsw, nss = E.ea_msg_scales(ec.qw, d), E.ea_msg_scales(ec.qs, d)
+    ww = E.ea_msg_words(ec.qw, d)
+    ws = gd.wrap("workspace", rb.workspace)
+    rows = []
+    for i in range(N):
+        rows.append({k: gd.wrap(f"{k}[{i}]", None if getattr(rb, k) is None else getattr(rb, k)[i].contiguous())
+                     for k in ("g", "e_w", "m_w", "v_w")})
+        rows[i]["codes"] = gd.wrap(f"wcodes[{i}]", torch.zeros(ww, dtype=torch.uint64, device="cuda"))
+        rows[i]["scales"] = gd.wrap(f"wscales[{i}]", torch.zeros(nsw, dtype=torch.float32, device="cuda")) \
+            if nsw else None
+    wcodes = gd.wrap("wcodes", torch.zeros((N, ww), dtype=torch.uint64, device="cuda"))
+    wscales = gd.wrap("wscales", torch.zeros((N, nsw), dtype=torch.float32, device="cuda")) if nsw else None
+    m, v, u = gd.wrap("m", rb.m), gd.wrap("v", rb.v), gd.wrap("u", rb.u)
+    e_s, x = gd.wrap("e_s", rb.e_s), gd.wrap("x", rb.x)
+    scodes = gd.wrap("scodes", rb.scodes)
+    sscales = gd.wrap("sscales", rb.sscales[:nss].contiguous()) if nss else None
+    for t in (1, 2):
+        for i, r in enumerate(rows):
+            E.ea_worker_compress(ec, i, t, r["g"], r["e_w"], r["m_w"], r["v_w"], r["codes"], r["scales"], ws)
+            wcodes[i].copy_(r["codes"])
+            if nsw:
+                wscales[i].copy_(r["scales"])
+        E.ea_server_aggregate_adam(ec, t, wcodes, wscales, m, v, u)
+        E.ea_server_compress(ec, t, u, e_s, scodes, sscales, ws)
+        E.ea_worker_apply(ec, scodes, sscales, x)
 
 
 @pytest.mark.parametrize("d,N", [(500, 10), (65, 2), (777, 31), (4096, 3)])
