@@ -31,14 +31,15 @@ PATTERN = 0xA5
 class Guarded:
     """Tensors viewed from the front of larger pattern-filled allocations."""
 
-    def __init__(self):
+    def __init__(self, pattern=PATTERN):
         self.bufs = {}
+        self.pattern = pattern
 
     def wrap(self, name, t):
         if t is None:
             return None
         nbytes = t.numel() * t.element_size()
-        big = torch.full((nbytes + GUARD,), PATTERN, dtype=torch.uint8, device="cuda")
+        big = torch.full((nbytes + GUARD,), self.pattern, dtype=torch.uint8, device="cuda")
         view = big[:nbytes].view(t.dtype).view(t.shape)
         view.copy_(t)
         self.bufs[name] = (big, nbytes)
@@ -48,7 +49,7 @@ class Guarded:
         torch.cuda.synchronize()
         for name, (big, nbytes) in self.bufs.items():
             tail = big[nbytes:]
-            bad = int((tail != PATTERN).sum().item())
+            bad = int((tail != self.pattern).sum().item())
             assert bad == 0, f"{what}: {bad} bytes written past the end of {name} ({nbytes} bytes)"
 
 
@@ -162,3 +163,31 @@ def test_toy_writes_stay_in_bounds(d, N):
                       st["wcodes"], st["scodes"], gs, g, ws)
     E.ea_toy_grad(d, N, A, xs, xi, st["x"], g, gs, ws)
     gd.check(f"toy d={d} N={N}")
+
+
+@pytest.mark.parametrize("name,d,N,q,placement", ROUNDS, ids=[r[0] for r in ROUNDS])
+def test_round_reads_stay_in_bounds(name, d, N, q, placement):
+    """The same two rounds from ordinary allocations and from allocations
+    whose bytes past every array are 0xFF (a NaN in binary32): every output
+    agrees bit for bit, so no read past an array's end reaches a result."""
+    _, ec = configs(d, N, q, q, placement, seed=3)
+    rng = np.random.default_rng(d * 3 + N)
+    g0 = torch.from_numpy((rng.standard_normal((N, d)) * 1e-2).astype(np.float32)).cuda()
+    outs = []
+    for pattern in (None, 0xFF):
+        rb = allocate(ec)
+        init_state(ec, rb)
+        rb.g.copy_(g0)
+        if pattern is None:
+            args = rb.step_args()
+            nsw, nss = E.ea_msg_scales(ec.qw, d), E.ea_msg_scales(ec.qs, d)
+            args["wscales"] = args["wscales"][:, :nsw].contiguous() if nsw else None
+            args["sscales"] = args["sscales"][:nss].contiguous() if nss else None
+        else:
+            args = _step_args(ec, rb, Guarded(pattern))
+        for t in (1, 2):
+            E.ea_step(ec, t, **args)
+        torch.cuda.synchronize()
+        outs.append({k: v.clone() for k, v in args.items() if v is not None and k not in ("g", "workspace")})
+    for k in outs[0]:
+        assert torch.equal(outs[0][k].view(torch.uint8), outs[1][k].view(torch.uint8)), f"{name}: {k}"
