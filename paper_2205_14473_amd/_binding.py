@@ -10,7 +10,9 @@ import ctypes as C
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libea.so")
+# EA_LIB names another build of the same sources to load instead (the host
+# code built with sanitizers, for the CPU tests); it must exist.
+LIB_PATH = os.environ.get("EA_LIB") or os.path.join(PKG, "libea.so")
 
 EA_OK, EA_ERR_ARG, EA_ERR_ALIGN, EA_ERR_HIP, EA_ERR_UNSUPPORTED = 0, -1, -2, -3, -4
 EA_Q_NONE, EA_Q_SCALED_SIGN, EA_Q_STOCH_UNIFORM, EA_Q_DET_UNIFORM, EA_Q_POW2, EA_Q_TOPK, EA_Q_RANDK = 0, 1, 2, 3, 4, 5, 6

@@ -75,6 +75,37 @@ def build(verbose: bool = False, extra=()) -> str:
     return LIB
 
 
+# The host code (argument checks, planning, launch set-up) built with
+# AddressSanitizer and UndefinedBehaviorSanitizer for the CPU tests; device
+# code is unchanged (the last build's device objects are reused).  The
+# library is linked without the sanitizer runtime: the process that loads it
+# preloads clang's.
+SAN_HOST_FLAGS = ["-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-sanitize-recover=all",
+                  "-fno-omit-frame-pointer"]
+
+
+def build_host_sanitized(outdir: str, verbose: bool = False) -> str:
+    """Host passes of every source with SAN_HOST_FLAGS into outdir, then one
+    link; needs the device objects of build().  Returns the library's path."""
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(outdir, exist_ok=True)
+    host, objs = [], []
+    for src in SOURCES:
+        bn = os.path.basename(src)
+        fb = os.path.join(objdir, bn + ".hipfb")
+        if not os.path.exists(fb):
+            raise FileNotFoundError(f"{fb}: run build() first")
+        cuid = "-cuid=" + hashlib.sha256(bn.encode()).hexdigest()[:16]
+        o = os.path.join(outdir, bn + ".o")
+        host.append([CLANG, *FLAGS, cuid, *SAN_HOST_FLAGS, "--cuda-host-only", "-c", "-Xclang",
+                     "-fcuda-include-gpubinary", "-Xclang", fb, src, "-o", o])
+        objs.append(o)
+    _run_all(host, verbose)
+    lib = os.path.join(outdir, "libea.so")
+    subprocess.run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", lib], check=True)
+    return lib
+
+
 def is_stale() -> bool:
     if not os.path.exists(LIB):
         return True
