@@ -1,4 +1,4 @@
-"""The host ABI tests run again against the library's host code built with
+"""The host ABI and benchmark host tests run again against the library's host code built with
 AddressSanitizer and UndefinedBehaviorSanitizer (any finding aborts): the
 argument checks, the quantizer validation fuzz, the message and workspace
 size arithmetic and the launch planning reach no out-of-bounds access, no
@@ -40,7 +40,8 @@ def test_abi_host_tests_pass_under_sanitizers(tmp_path):
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
     assert r.returncode == 0 and r.stdout.strip() == lib, r.stdout + r.stderr
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider", "-m", "not gpu",
-                        os.path.join(HERE, "test_abi_host.py")], cwd=ROOT, env=env, capture_output=True, text=True,
+                        os.path.join(HERE, "test_abi_host.py"), os.path.join(HERE, "test_bench_host.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True,
                        timeout=900)
     out = r.stdout + r.stderr
     for f in sorted(tmp_path.glob("findings*")):
