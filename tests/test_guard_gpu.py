@@ -191,3 +191,41 @@ def test_round_reads_stay_in_bounds(name, d, N, q, placement):
         outs.append({k: v.clone() for k, v in args.items() if v is not None and k not in ("g", "workspace")})
     for k in outs[0]:
         assert torch.equal(outs[0][k].view(torch.uint8), outs[1][k].view(torch.uint8)), f"{name}: {k}"
+
+
+@pytest.mark.parametrize("d,N", [(500, 10), (65, 2), (777, 31), (4096, 3)])
+def test_toy_reads_stay_in_bounds(d, N):
+    """Two toy steps and one ea_toy_grad from ordinary allocations and from
+    allocations with NaN bytes past every array (A, x*, xi, the state, the
+    workspace): the same bits everywhere, so no read past an array's end
+    reaches a gradient, a norm or the round."""
+    rng = np.random.default_rng(d + 7)
+    A0 = torch.from_numpy(rng.standard_normal((d, d)).astype(np.float32)).cuda()
+    xs0 = torch.from_numpy((rng.standard_normal(d) * math.sqrt(0.1)).astype(np.float32)).cuda()
+    xi0 = torch.from_numpy((rng.standard_normal((N, d)) * math.sqrt(0.1)).astype(np.float32)).cuda()
+    ex2 = qfields(O.Q_POW2, kmin=-17, kmax=-11)
+    _, ec = configs(d, N, ex2, ex2, O.ADAM_AT_WORKER, seed=9, beta1=0.9, beta2=0.99, lr=1e-4)
+    outs = []
+    for pattern in (None, 0xFF):
+        rb = allocate(ec)
+        init_state(ec, rb)
+        rb.x.copy_(xs0 * 0.5)
+        gd = Guarded(pattern if pattern is not None else PATTERN)
+        w = (lambda k, t: t) if pattern is None else gd.wrap
+        A, xs, xi = w("A", A0.clone()), w("xs", xs0.clone()), w("xi", xi0.clone())
+        st = {k: w(k, getattr(rb, k)) for k in ("e_w", "m_w", "v_w", "e_s", "x", "wcodes", "scodes")}
+        ws = w("workspace", torch.zeros(E.ea_toy_workspace_bytes(d), dtype=torch.uint8, device="cuda"))
+        g = w("g", torch.zeros((N, d), dtype=torch.float32, device="cuda"))
+        gs = w("grad_sq", torch.zeros(1, dtype=torch.float64, device="cuda"))
+        for t in (1, 2):
+            E.ea_toy_step(ec, t, A, xs, xi, st["e_w"], st["m_w"], st["v_w"], None, None, st["e_s"], st["x"],
+                          st["wcodes"], st["scodes"], gs, g, ws)
+        g2 = w("g2", torch.zeros((N, d), dtype=torch.float32, device="cuda"))
+        gs2 = w("grad_sq2", torch.zeros(1, dtype=torch.float64, device="cuda"))
+        E.ea_toy_grad(d, N, A, xs, xi, st["x"], g2, gs2, ws)
+        torch.cuda.synchronize()
+        res = {k: v.clone() for k, v in st.items()}
+        res.update(g=g.clone(), gs=gs.clone(), g2=g2.clone(), gs2=gs2.clone())
+        outs.append(res)
+    for k in outs[0]:
+        assert torch.equal(outs[0][k].view(torch.uint8), outs[1][k].view(torch.uint8)), f"toy d={d} N={N}: {k}"
