@@ -71,7 +71,8 @@ ROUNDS = [
     ("ex1-wide", 777, 17, qfields(O.Q_DET_UNIFORM, 3, bucket=2048), O.ADAM_AT_SERVER),
     ("stoch2-max-wide", 9000, 8, qfields(O.Q_STOCH_UNIFORM, 2, O.SCALE_MAX, bucket=2048), O.ADAM_AT_WORKER),
     ("raw", 1000, 2, qfields(O.Q_NONE), O.ADAM_AT_SERVER),
-    ("randk-short-bucket", 1500, 3, dict(kind=O.Q_RANDK, keep=40, bucket=2048, error_feedback=1), O.ADAM_AT_WORKER),
+    ("randk-short-bucket", 1500, 3, dict(kind=O.Q_RANDK, keep=40, bucket=2048, error_feedback=1),
+     O.ADAM_AT_WORKER),
 ]
 
 
